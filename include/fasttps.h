@@ -1,0 +1,156 @@
+/*
+ * fasttps.h -- C ABI of the FastTPS token-phase decoder layer for MI355X (gfx950).
+ *
+ * One call of fasttps_decode_step runs one decode step of one pre-norm decoder
+ * layer for B sequences, each holding one new token (the token phase of the
+ * FastTPS paper, Section 2.1: B x N x D activations with N = 1):
+ *
+ *   h  = RMSNorm1(x)                              (Section 2.3 step 1, Alg. 4)
+ *   q, k, v = W_q h, W_k h, W_v h                 (Section 2.2)
+ *   q, k = RoPE(q, k) at position N_p             (Alg. 3, joint RoPE; Eq. 22)
+ *   K_cache[b, g, N_p] = bf16(k), V_cache[b, g, N_p] = bf16(v)
+ *                                                 (GKVC in-place append, Eq. 1)
+ *   o  = softmax(q K^T / sqrt(d)) V over the N_p + 1 entries  (Eq. 25-28)
+ *   h1 = x + W_o o
+ *   y  = h1 + W_down (SiLU(W_gate h2) * (W_up h2)),  h2 = RMSNorm2(h1)
+ *                                                 (Eq. mlp_main; Alg. 4, Eq. 29-32)
+ *
+ * Conventions
+ *   - Tensors are bfloat16 (bit patterns in uint16 storage) unless stated.
+ *   - "device" pointers are HIP device addresses on the current device;
+ *     "host" pointers are ordinary CPU memory.
+ *   - Weight matrices use the [out, in] row-major layout of nn.Linear.
+ *   - Caches are [B_max, H_kv, N_max, d] row-major, contiguous; the slot of
+ *     (b, g, n) is at element ((b * H_kv + g) * N_max + n) * d  (Eq. 1 with
+ *     N_p + N_r = N_max).
+ *   - Every function returns FASTTPS_OK (0) or a negative status. No
+ *     exception or abort crosses the ABI. All argument checks happen before
+ *     the first HIP call, so a rejected call has no side effect. The text of
+ *     the last error on the calling thread is given by fasttps_last_error().
+ *   - Streams are hipStream_t passed as void*; NULL means the default stream.
+ */
+#ifndef FASTTPS_H
+#define FASTTPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define FASTTPS_API __attribute__((visibility("default")))
+#else
+#define FASTTPS_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define FASTTPS_OK                0
+#define FASTTPS_ERR_INVALID_ARG  -1  /* null pointer, size out of range, overlap */
+#define FASTTPS_ERR_UNSUPPORTED  -2  /* shape the kernels are not built for */
+#define FASTTPS_ERR_ALIGNMENT    -3  /* a tensor pointer is not 16-byte aligned */
+#define FASTTPS_ERR_CACHE_FULL   -4  /* some pos[b] >= N_max (N_r = 0) or pos[b] < 0 */
+#define FASTTPS_ERR_OOM          -5  /* device allocation failed */
+#define FASTTPS_ERR_HIP          -6  /* a HIP runtime call failed (text in last_error) */
+#define FASTTPS_ERR_BAD_HANDLE   -7  /* handle null, destroyed, or of another layer */
+
+typedef struct fasttps_layer fasttps_layer;      /* config, scratch, RoPE table */
+typedef struct fasttps_weights fasttps_weights;  /* packed weights of one layer */
+
+/* Shape of one decoder layer. */
+typedef struct {
+  int32_t hidden;        /* D; multiple of 8, 8 <= D <= 8192 */
+  int32_t n_heads;       /* H query heads; H / H_kv in {1, 2, 4}; H * d <= 8192 */
+  int32_t n_kv_heads;    /* H_kv */
+  int32_t head_dim;      /* d in {64, 96, 128} */
+  int32_t intermediate;  /* K (MLP width); multiple of 8, <= 65536 */
+  int32_t max_batch;     /* B_max in [1, 64] */
+  int32_t max_seq;       /* N_max = N_p + N_r: cache capacity per sequence (Eq. 1), >= 1 */
+  float rope_base;       /* RoPE base (e.g. 1e4, 5e5); angle_j(n) = n * base^(-2j/d) */
+  float rms_eps;         /* RMSNorm epsilon, added inside the square root, > 0 */
+} fasttps_config;
+
+/* Raw weights of one layer: device pointers, bf16, nn.Linear layout. */
+typedef struct {
+  const void* attn_norm;  /* [D]        gain of RMSNorm1 */
+  const void* w_q;        /* [H*d, D]   */
+  const void* w_k;        /* [H_kv*d, D] */
+  const void* w_v;        /* [H_kv*d, D] */
+  const void* w_o;        /* [D, H*d]   */
+  const void* mlp_norm;   /* [D]        gain of RMSNorm2 */
+  const void* w_gate;     /* [K, D]     */
+  const void* w_up;       /* [K, D]     */
+  const void* w_down;     /* [D, K]     */
+} fasttps_weights_desc;
+
+/* Create a layer handle on the current device: validates the config,
+ * allocates the step's scratch (sized for max_batch) and builds the RoPE
+ * cos/sin table for positions [0, N_max) (computed in double precision on the
+ * host; the paper feeds sin/cos to RoPE as inputs, Alg. 1 and Alg. 3).
+ * The handle owns its memory until fasttps_layer_destroy. Blocking. */
+FASTTPS_API int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out);
+
+/* Pack one layer's raw weights into the library's layout: fused [W_q; W_k;
+ * W_v] rows, interlaced gate/up rows (Section 3.2 item 1, Alg. 4: tiles of
+ * gate rows alternate with the matching up rows), and W_down transposed to
+ * [K, D] so each MLP block streams its own K-slice. Runs on `stream` and
+ * returns once the copies are complete; the raw weights may then be freed.
+ * The packed weights belong to the returned handle (free with
+ * fasttps_weights_free) and may be used with any layer handle of the same
+ * config. */
+FASTTPS_API int fasttps_weights_pack(fasttps_layer* layer, const fasttps_weights_desc* w,
+                         void* stream, fasttps_weights** out);
+
+/* One decode step (see the top of this file).
+ *   x        device, [batch, D] bf16 input token activations
+ *   pos      host, [batch] int32: N_p of each sequence = index of the new
+ *            token = number of valid cache entries before the call
+ *   batch    number of sequences, 1 <= batch <= max_batch
+ *   k_cache, v_cache
+ *            device, [batch, H_kv, N_max, d] bf16 (a leading block of a
+ *            [B_max, ...] cache is fine). Entries [0, pos[b]) are read; the
+ *            one slot pos[b] of every (b, g) is written; nothing else is read
+ *            or written. After the call the caller's length is pos[b] + 1
+ *            (Section 3.1.1: N_p <- N_p + 1, N_r <- N_r - 1).
+ *   y        device, [batch, D] bf16 output; must not overlap x or the caches
+ *   stream   the step is enqueued on this stream; the call neither allocates
+ *            nor synchronizes.
+ * All tensors must be 16-byte aligned. A handle's scratch is shared by its
+ * calls, so steps on one handle must not run concurrently on different
+ * streams. */
+FASTTPS_API int fasttps_decode_step(fasttps_layer* layer, const fasttps_weights* w, const void* x,
+                        const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
+                        void* y, void* stream);
+
+/* Test hook: copy one of the step's fp32 intermediates from the handle's
+ * scratch into `dst` (device), on `stream`, after a fasttps_decode_step on the
+ * same stream. `which` selects:
+ *   FASTTPS_DBG_QKV   [batch, (H + 2 H_kv) d]  q | k | v before RoPE
+ *   FASTTPS_DBG_ATTN  [batch, H d]             attention output o
+ *   FASTTPS_DBG_H1    [batch, D]               x + W_o o
+ *   FASTTPS_DBG_MLP_A [batch, K]               SiLU(gate) * up (written only
+ *                                               when fasttps_set_debug(layer, 1))
+ * `bytes` must equal the size of the selected buffer for `batch`. */
+#define FASTTPS_DBG_QKV   0
+#define FASTTPS_DBG_ATTN  1
+#define FASTTPS_DBG_H1    2
+#define FASTTPS_DBG_MLP_A 3
+FASTTPS_API int fasttps_debug_read(fasttps_layer* layer, int32_t which, int32_t batch, void* dst,
+                       size_t bytes, void* stream);
+
+/* Test hook: when enabled, steps also store the MLP intermediate a. */
+FASTTPS_API int fasttps_set_debug(fasttps_layer* layer, int32_t enable);
+
+FASTTPS_API int fasttps_weights_free(fasttps_weights* w);
+FASTTPS_API int fasttps_layer_destroy(fasttps_layer* layer);
+
+/* Static text of a status code. */
+FASTTPS_API const char* fasttps_status_string(int status);
+/* Text of the last error on the calling thread ("" if none). */
+FASTTPS_API const char* fasttps_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FASTTPS_H */

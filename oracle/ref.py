@@ -35,11 +35,29 @@ BF16_MAX = float.fromhex("0x1.fep127")  # largest finite bfloat16, bit pattern 0
 # bfloat16 storage boundary
 # ---------------------------------------------------------------------------
 
-def bf16_bits_to_f64(bits) -> np.ndarray:
-    """Exact value of bf16 bit patterns (bfloat16 is the top half of binary32)."""
-    b = np.asarray(bits, dtype=np.uint16)
+def _widen_chunk(b: np.ndarray, out: np.ndarray) -> None:
     with np.errstate(invalid="ignore"):
-        return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+        out[...] = (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def bf16_bits_to_f64(bits) -> np.ndarray:
+    """Exact value of bf16 bit patterns (bfloat16 is the top half of binary32).
+
+    Large arrays are widened in slices on a few threads; the result does not
+    depend on the slicing (each element is converted on its own).
+    """
+    b = np.ascontiguousarray(np.asarray(bits, dtype=np.uint16))
+    out = np.empty(b.shape, dtype=np.float64)
+    n = b.size
+    if n < (1 << 22):
+        _widen_chunk(b, out)
+        return out
+    from concurrent.futures import ThreadPoolExecutor
+    fb, fo = b.reshape(-1), out.reshape(-1)
+    step = 1 << 21
+    with ThreadPoolExecutor(max_workers=8) as ex:
+        list(ex.map(lambda i: _widen_chunk(fb[i:i + step], fo[i:i + step]), range(0, n, step)))
+    return out
 
 
 def f64_to_bf16_bits(x) -> np.ndarray:

@@ -1,0 +1,95 @@
+// Device helpers shared by the gfx950 kernels of the FastTPS decode layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fasttps {
+
+constexpr int kWave = 64;
+
+// ---- bfloat16 <-> float -------------------------------------------------
+// bf16 is the upper half of a binary32, so widening is a shift.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// float -> bf16, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x0040u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// double -> bf16 with a single rounding (nearest even): first to float with
+// round-to-odd (truncate, then set the last bit if anything was dropped),
+// which keeps the information a second nearest-even rounding needs because
+// float carries 16 more significand bits than bf16.
+__device__ __forceinline__ uint16_t f64_to_bf16(double x) {
+  float t = __double2float_rz(x);
+  uint32_t u = __float_as_uint(t);
+  if ((double)t != x && x == x) u |= 1u;
+  return f32_to_bf16(__uint_as_float(u));
+}
+
+// Eight bf16 (one 16-byte load) dotted with eight floats.
+__device__ __forceinline__ float dot8(const uint4 w, const float* h) {
+  float s = bf16_lo(w.x) * h[0];
+  s = fmaf(bf16_hi(w.x), h[1], s);
+  s = fmaf(bf16_lo(w.y), h[2], s);
+  s = fmaf(bf16_hi(w.y), h[3], s);
+  s = fmaf(bf16_lo(w.z), h[4], s);
+  s = fmaf(bf16_hi(w.z), h[5], s);
+  s = fmaf(bf16_lo(w.w), h[6], s);
+  s = fmaf(bf16_hi(w.w), h[7], s);
+  return s;
+}
+
+__device__ __forceinline__ float fma8(const uint4 w, const float* h, float acc) {
+  acc = fmaf(bf16_lo(w.x), h[0], acc);
+  acc = fmaf(bf16_hi(w.x), h[1], acc);
+  acc = fmaf(bf16_lo(w.y), h[2], acc);
+  acc = fmaf(bf16_hi(w.y), h[3], acc);
+  acc = fmaf(bf16_lo(w.z), h[4], acc);
+  acc = fmaf(bf16_hi(w.z), h[5], acc);
+  acc = fmaf(bf16_lo(w.w), h[6], acc);
+  acc = fmaf(bf16_hi(w.w), h[7], acc);
+  return acc;
+}
+
+__device__ __forceinline__ void unpack8(const uint4 w, float* f) {
+  f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x);
+  f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
+  f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z);
+  f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
+}
+
+// ---- wavefront reductions (64 lanes) ------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
+// Sum of x*x over n bf16 values of a row, for the whole block; every thread
+// gets the total. `red` must hold blockDim.x / 64 floats.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+  const int nw = blockDim.x / kWave;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+}  // namespace fasttps

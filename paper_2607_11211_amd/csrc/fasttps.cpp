@@ -1,0 +1,477 @@
+// C ABI of the FastTPS decode layer: validation, ownership, launch sequence.
+#include "fasttps.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace fasttps;
+
+namespace {
+
+constexpr uint64_t kLayerMagic = 0x4641535454505331ull;    // "FASTTPS1"
+constexpr uint64_t kWeightsMagic = 0x4641535454505357ull;  // "FASTTPSW"
+constexpr uint64_t kDeadMagic = 0xDEADDEADDEADDEADull;
+constexpr int kTargetAttnBlocks = 1024;  // ~4 blocks per CU on 256 CUs
+constexpr int kAttnTile = 64;
+constexpr int kMaxSplits = 256;
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(FASTTPS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+int round_up(int v, int m) { return (v + m - 1) / m * m; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+int mlp_tile(int inter) { return round_up(ceil_div(inter, 256), 8); }
+
+}  // namespace
+
+struct fasttps_layer {
+  uint64_t magic;
+  fasttps_config cfg;
+  int device;
+  int tk, nblk_mlp, nsplit_cap, debug;
+  void* arena;
+  double* rope_cos;
+  double* rope_sin;
+  float* qkv;
+  float* attn_part;
+  unsigned* tickets;
+  float* attn_o;
+  float* h1;
+  float* mlp_part;
+  float* mlp_a;
+};
+
+struct fasttps_weights {
+  uint64_t magic;
+  fasttps_config cfg;
+  int tk;
+  void* arena;
+  uint16_t* w_qkv;
+  uint16_t* w_o;
+  uint16_t* w_gu;
+  uint16_t* w_downT;
+  uint16_t* attn_norm;
+  uint16_t* mlp_norm;
+};
+
+namespace {
+
+int validate_config(const fasttps_config* c) {
+  if (!c) return fail(FASTTPS_ERR_INVALID_ARG, "config is null");
+  if (c->hidden <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 || c->intermediate <= 0 ||
+      c->max_batch <= 0 || c->max_seq <= 0)
+    return fail(FASTTPS_ERR_INVALID_ARG, "config sizes must be positive");
+  if (c->max_batch > kMaxBatch) return fail(FASTTPS_ERR_INVALID_ARG, "max_batch %d > %d", c->max_batch, kMaxBatch);
+  if (!(std::isfinite(c->rope_base) && c->rope_base > 1.0f))
+    return fail(FASTTPS_ERR_INVALID_ARG, "rope_base must be finite and > 1");
+  if (!(std::isfinite(c->rms_eps) && c->rms_eps > 0.0f))
+    return fail(FASTTPS_ERR_INVALID_ARG, "rms_eps must be finite and > 0");
+  if (c->hidden % 8 != 0 || c->hidden > 8192)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "hidden %d: need a multiple of 8 up to 8192", c->hidden);
+  if (c->head_dim != 64 && c->head_dim != 96 && c->head_dim != 128)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "head_dim %d: supported 64, 96, 128", c->head_dim);
+  if (c->n_heads % c->n_kv_heads != 0) return fail(FASTTPS_ERR_UNSUPPORTED, "n_heads %% n_kv_heads != 0");
+  const int group = c->n_heads / c->n_kv_heads;
+  if (group != 1 && group != 2 && group != 4)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "n_heads / n_kv_heads = %d: supported 1, 2, 4", group);
+  if ((long)c->n_heads * c->head_dim > 8192)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "n_heads * head_dim > 8192");
+  if (c->intermediate % 8 != 0 || c->intermediate > 65536)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "intermediate %d: need a multiple of 8 up to 65536", c->intermediate);
+  if ((long)c->max_seq * c->head_dim * c->n_kv_heads * c->max_batch > (1L << 40))
+    return fail(FASTTPS_ERR_UNSUPPORTED, "cache too large");
+  return FASTTPS_OK;
+}
+
+bool same_shape(const fasttps_config& a, const fasttps_config& b) {
+  return a.hidden == b.hidden && a.n_heads == b.n_heads && a.n_kv_heads == b.n_kv_heads &&
+         a.head_dim == b.head_dim && a.intermediate == b.intermediate;
+}
+
+// Live handles: a handle is dereferenced only after it is found here, so a
+// stale or foreign pointer is reported instead of read.
+std::mutex g_handles_mu;
+std::unordered_set<const void*> g_layers, g_weights;
+
+void track(std::unordered_set<const void*>& set, const void* p, bool add) {
+  std::lock_guard<std::mutex> lk(g_handles_mu);
+  if (add)
+    set.insert(p);
+  else
+    set.erase(p);
+}
+
+bool live(const std::unordered_set<const void*>& set, const void* p) {
+  std::lock_guard<std::mutex> lk(g_handles_mu);
+  return p && set.count(p) != 0;
+}
+
+bool layer_ok(const fasttps_layer* l) { return live(g_layers, l) && l->magic == kLayerMagic; }
+bool weights_ok(const fasttps_weights* w) { return live(g_weights, w) && w->magic == kWeightsMagic; }
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+}  // namespace
+
+extern "C" {
+
+const char* fasttps_status_string(int status) {
+  switch (status) {
+    case FASTTPS_OK: return "ok";
+    case FASTTPS_ERR_INVALID_ARG: return "invalid argument";
+    case FASTTPS_ERR_UNSUPPORTED: return "unsupported shape";
+    case FASTTPS_ERR_ALIGNMENT: return "pointer not 16-byte aligned";
+    case FASTTPS_ERR_CACHE_FULL: return "cache full or bad position";
+    case FASTTPS_ERR_OOM: return "device allocation failed";
+    case FASTTPS_ERR_HIP: return "HIP runtime error";
+    case FASTTPS_ERR_BAD_HANDLE: return "bad handle";
+    default: return "unknown status";
+  }
+}
+
+const char* fasttps_last_error(void) { return g_last_error.c_str(); }
+
+int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
+  g_last_error.clear();
+  if (!out) return fail(FASTTPS_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  int st = validate_config(cfg);
+  if (st) return st;
+  const fasttps_config c = *cfg;
+  const int d = c.head_dim, half = d / 2;
+  const int B = c.max_batch;
+  const int tk = mlp_tile(c.intermediate);
+  const int nblk = ceil_div(c.intermediate, tk);
+  const int nsplit_cap = std::min({kMaxSplits, ceil_div(kTargetAttnBlocks, c.n_kv_heads), ceil_div(c.max_seq, kAttnTile)});
+  const size_t qkv_rows = (size_t)(c.n_heads + 2 * c.n_kv_heads) * d;
+
+  // RoPE table in double precision: angle(n, j) = n * base^(-2j/d)
+  std::vector<double> cs((size_t)c.max_seq * half), sn((size_t)c.max_seq * half);
+  for (int j = 0; j < half; ++j) {
+    const double inv_freq = std::pow((double)c.rope_base, -2.0 * (double)j / (double)d);
+    for (int n = 0; n < c.max_seq; ++n) {
+      const double th = (double)n * inv_freq;
+      cs[(size_t)n * half + j] = std::cos(th);
+      sn[(size_t)n * half + j] = std::sin(th);
+    }
+  }
+
+  size_t sizes[9] = {
+      cs.size() * sizeof(double),
+      sn.size() * sizeof(double),
+      (size_t)B * qkv_rows * sizeof(float),
+      (size_t)B * c.n_heads * nsplit_cap * (d + 2) * sizeof(float),
+      (size_t)B * c.n_kv_heads * sizeof(unsigned),
+      (size_t)B * c.n_heads * d * sizeof(float),
+      (size_t)B * c.hidden * sizeof(float),
+      (size_t)nblk * B * c.hidden * sizeof(float),
+      (size_t)B * c.intermediate * sizeof(float),
+  };
+  size_t total = 0, offs[9];
+  for (int i = 0; i < 9; ++i) {
+    offs[i] = total;
+    total += align256(sizes[i]);
+  }
+
+  fasttps_layer* l = new (std::nothrow) fasttps_layer();
+  if (!l) return fail(FASTTPS_ERR_OOM, "host allocation failed");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    delete l;
+    return hip_fail(e, "hipGetDevice");
+  }
+  void* arena = nullptr;
+  e = hipMalloc(&arena, total);
+  if (e != hipSuccess) {
+    delete l;
+    (void)hipGetLastError();
+    return fail(FASTTPS_ERR_OOM, "hipMalloc(%zu): %s", total, hipGetErrorString(e));
+  }
+  char* base = static_cast<char*>(arena);
+  l->magic = kLayerMagic;
+  l->cfg = c;
+  l->device = dev;
+  l->tk = tk;
+  l->nblk_mlp = nblk;
+  l->nsplit_cap = nsplit_cap;
+  l->debug = 0;
+  l->arena = arena;
+  l->rope_cos = reinterpret_cast<double*>(base + offs[0]);
+  l->rope_sin = reinterpret_cast<double*>(base + offs[1]);
+  l->qkv = reinterpret_cast<float*>(base + offs[2]);
+  l->attn_part = reinterpret_cast<float*>(base + offs[3]);
+  l->tickets = reinterpret_cast<unsigned*>(base + offs[4]);
+  l->attn_o = reinterpret_cast<float*>(base + offs[5]);
+  l->h1 = reinterpret_cast<float*>(base + offs[6]);
+  l->mlp_part = reinterpret_cast<float*>(base + offs[7]);
+  l->mlp_a = reinterpret_cast<float*>(base + offs[8]);
+
+  if ((e = hipMemcpy(l->rope_cos, cs.data(), sizes[0], hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(l->rope_sin, sn.data(), sizes[1], hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemset(l->tickets, 0, sizes[4])) != hipSuccess ||
+      (e = hipMemset(l->mlp_a, 0, sizes[8])) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) {
+    (void)hipFree(arena);
+    l->magic = kDeadMagic;
+    delete l;
+    return hip_fail(e, "layer setup");
+  }
+  track(g_layers, l, true);
+  *out = l;
+  return FASTTPS_OK;
+}
+
+int fasttps_layer_destroy(fasttps_layer* l) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "layer handle is null or already destroyed");
+  track(g_layers, l, false);
+  l->magic = kDeadMagic;
+  hipError_t e = hipFree(l->arena);
+  delete l;
+  if (e != hipSuccess) return hip_fail(e, "hipFree");
+  return FASTTPS_OK;
+}
+
+int fasttps_set_debug(fasttps_layer* l, int32_t enable) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  l->debug = enable ? 1 : 0;
+  return FASTTPS_OK;
+}
+
+int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* stream, fasttps_weights** out) {
+  g_last_error.clear();
+  if (!out) return fail(FASTTPS_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (!w) return fail(FASTTPS_ERR_INVALID_ARG, "weights descriptor is null");
+  const void* ptrs[9] = {w->attn_norm, w->w_q, w->w_k, w->w_v, w->w_o, w->mlp_norm, w->w_gate, w->w_up, w->w_down};
+  for (int i = 0; i < 9; ++i) {
+    if (!ptrs[i]) return fail(FASTTPS_ERR_INVALID_ARG, "weight pointer %d is null", i);
+    if (!aligned16(ptrs[i])) return fail(FASTTPS_ERR_ALIGNMENT, "weight pointer %d is not 16-byte aligned", i);
+  }
+  const fasttps_config& c = l->cfg;
+  const size_t D = c.hidden, K = c.intermediate, d = c.head_dim;
+  const size_t q = (size_t)c.n_heads * d, kv = (size_t)c.n_kv_heads * d;
+  const size_t n_qkv = (q + 2 * kv) * D, n_o = D * q, n_gu = 2 * K * D, n_d = K * D;
+  size_t offs[6], sizes[6] = {n_qkv * 2, n_o * 2, n_gu * 2, n_d * 2, D * 2, D * 2}, total = 0;
+  for (int i = 0; i < 6; ++i) {
+    offs[i] = total;
+    total += align256(sizes[i]);
+  }
+  fasttps_weights* pw = new (std::nothrow) fasttps_weights();
+  if (!pw) return fail(FASTTPS_ERR_OOM, "host allocation failed");
+  void* arena = nullptr;
+  hipError_t e = hipMalloc(&arena, total);
+  if (e != hipSuccess) {
+    delete pw;
+    (void)hipGetLastError();
+    return fail(FASTTPS_ERR_OOM, "hipMalloc(%zu): %s", total, hipGetErrorString(e));
+  }
+  char* base = static_cast<char*>(arena);
+  pw->magic = kWeightsMagic;
+  pw->cfg = c;
+  pw->tk = l->tk;
+  pw->arena = arena;
+  pw->w_qkv = reinterpret_cast<uint16_t*>(base + offs[0]);
+  pw->w_o = reinterpret_cast<uint16_t*>(base + offs[1]);
+  pw->w_gu = reinterpret_cast<uint16_t*>(base + offs[2]);
+  pw->w_downT = reinterpret_cast<uint16_t*>(base + offs[3]);
+  pw->attn_norm = reinterpret_cast<uint16_t*>(base + offs[4]);
+  pw->mlp_norm = reinterpret_cast<uint16_t*>(base + offs[5]);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const auto* g = static_cast<const uint16_t*>(w->w_gate);
+  const auto* u = static_cast<const uint16_t*>(w->w_up);
+  if ((e = hipMemcpyAsync(pw->w_qkv, w->w_q, q * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(pw->w_qkv + q * D, w->w_k, kv * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(pw->w_qkv + (q + kv) * D, w->w_v, kv * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(pw->w_o, w->w_o, n_o * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(pw->attn_norm, w->attn_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(pw->mlp_norm, w->mlp_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, l->tk, s)) != hipSuccess ||
+      (e = launch_transpose_bf16(static_cast<const uint16_t*>(w->w_down), pw->w_downT, (int)D, (int)K, s)) !=
+          hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess) {
+    (void)hipStreamSynchronize(s);
+    (void)hipFree(arena);
+    pw->magic = kDeadMagic;
+    delete pw;
+    return hip_fail(e, "weight packing");
+  }
+  track(g_weights, pw, true);
+  *out = pw;
+  return FASTTPS_OK;
+}
+
+int fasttps_weights_free(fasttps_weights* w) {
+  g_last_error.clear();
+  if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "weights handle is null or already freed");
+  track(g_weights, w, false);
+  w->magic = kDeadMagic;
+  hipError_t e = hipFree(w->arena);
+  delete w;
+  if (e != hipSuccess) return hip_fail(e, "hipFree");
+  return FASTTPS_OK;
+}
+
+int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
+                        int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad weights handle");
+  const fasttps_config& c = l->cfg;
+  if (!same_shape(c, w->cfg) || w->tk != l->tk)
+    return fail(FASTTPS_ERR_BAD_HANDLE, "weights were packed for another layer shape");
+  if (!x || !pos || !k_cache || !v_cache || !y) return fail(FASTTPS_ERR_INVALID_ARG, "null pointer argument");
+  if (batch < 1 || batch > c.max_batch)
+    return fail(FASTTPS_ERR_INVALID_ARG, "batch %d outside [1, %d]", batch, c.max_batch);
+  if (!aligned16(x) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(y))
+    return fail(FASTTPS_ERR_ALIGNMENT, "tensor pointers must be 16-byte aligned");
+  int maxp = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (pos[b] < 0 || pos[b] >= c.max_seq)
+      return fail(FASTTPS_ERR_CACHE_FULL, "pos[%d] = %d outside [0, %d)", b, pos[b], c.max_seq);
+    maxp = std::max(maxp, pos[b]);
+  }
+  const size_t D = c.hidden, d = c.head_dim;
+  const size_t act_bytes = (size_t)batch * D * 2;
+  const size_t cache_bytes = (size_t)batch * c.n_kv_heads * c.max_seq * d * 2;
+  if (overlaps(y, act_bytes, x, act_bytes) || overlaps(y, act_bytes, k_cache, cache_bytes) ||
+      overlaps(y, act_bytes, v_cache, cache_bytes))
+    return fail(FASTTPS_ERR_INVALID_ARG, "y overlaps x or a cache");
+  if (overlaps(k_cache, cache_bytes, v_cache, cache_bytes))
+    return fail(FASTTPS_ERR_INVALID_ARG, "k_cache and v_cache overlap");
+
+  // attention split: about kTargetAttnBlocks blocks, 64-position tiles
+  const int maxn = maxp + 1;
+  const int per_bg = ceil_div(kTargetAttnBlocks, batch * c.n_kv_heads);
+  int nsplit = std::min({per_bg, ceil_div(maxn, kAttnTile), l->nsplit_cap});
+  nsplit = std::max(nsplit, 1);
+  const int split_len = round_up(ceil_div(maxn, nsplit), kAttnTile);
+  nsplit = ceil_div(maxn, split_len);
+
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != l->device) return fail(FASTTPS_ERR_INVALID_ARG, "current device %d is not the layer's device %d", dev, l->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint16_t* xb = static_cast<const uint16_t*>(x);
+
+  GemvArgs qa{};
+  qa.w = w->w_qkv;
+  qa.rows = (c.n_heads + 2 * c.n_kv_heads) * (int)d;
+  qa.din = (int)D;
+  qa.batch = batch;
+  qa.x_bf16 = xb;
+  qa.gamma = w->attn_norm;
+  qa.out = l->qkv;
+  qa.eps = c.rms_eps;
+  if ((e = launch_rmsnorm_qkv(qa, s)) != hipSuccess) return hip_fail(e, "qkv launch");
+
+  AttnArgs aa{};
+  aa.qkv = l->qkv;
+  aa.rope_cos = l->rope_cos;
+  aa.rope_sin = l->rope_sin;
+  aa.k_cache = static_cast<uint16_t*>(k_cache);
+  aa.v_cache = static_cast<uint16_t*>(v_cache);
+  aa.part = l->attn_part;
+  aa.tickets = l->tickets;
+  aa.o = l->attn_o;
+  aa.batch = batch;
+  aa.n_heads = c.n_heads;
+  aa.n_kv_heads = c.n_kv_heads;
+  aa.head_dim = (int)d;
+  aa.max_seq = c.max_seq;
+  aa.split_len = split_len;
+  aa.nsplit = nsplit;
+  aa.nsplit_cap = l->nsplit_cap;
+  aa.scale = (float)(1.0 / std::sqrt((double)d));
+  for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
+  if ((e = launch_attention(aa, s)) != hipSuccess) return hip_fail(e, "attention launch");
+
+  GemvArgs oa{};
+  oa.w = w->w_o;
+  oa.rows = (int)D;
+  oa.din = c.n_heads * (int)d;
+  oa.batch = batch;
+  oa.x_bf16 = xb;
+  oa.in_f32 = l->attn_o;
+  oa.out = l->h1;
+  oa.eps = c.rms_eps;
+  if ((e = launch_oproj_residual(oa, s)) != hipSuccess) return hip_fail(e, "o-proj launch");
+
+  MlpArgs ma{};
+  ma.h1 = l->h1;
+  ma.gamma = w->mlp_norm;
+  ma.w_gu = w->w_gu;
+  ma.w_downT = w->w_downT;
+  ma.partial = l->mlp_part;
+  ma.a_dbg = l->debug ? l->mlp_a : nullptr;
+  ma.batch = batch;
+  ma.hidden = (int)D;
+  ma.inter = c.intermediate;
+  ma.tk = l->tk;
+  ma.eps = c.rms_eps;
+  if ((e = launch_mlp(ma, s)) != hipSuccess) return hip_fail(e, "mlp launch");
+  if ((e = launch_mlp_reduce(l->h1, l->mlp_part, l->nblk_mlp, batch, (int)D, static_cast<uint16_t*>(y), s)) !=
+      hipSuccess)
+    return hip_fail(e, "mlp reduce launch");
+  return FASTTPS_OK;
+}
+
+int fasttps_debug_read(fasttps_layer* l, int32_t which, int32_t batch, void* dst, size_t bytes, void* stream) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (!dst) return fail(FASTTPS_ERR_INVALID_ARG, "dst is null");
+  const fasttps_config& c = l->cfg;
+  if (batch < 1 || batch > c.max_batch) return fail(FASTTPS_ERR_INVALID_ARG, "batch out of range");
+  const void* src = nullptr;
+  size_t n = 0;
+  switch (which) {
+    case FASTTPS_DBG_QKV: src = l->qkv; n = (size_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim; break;
+    case FASTTPS_DBG_ATTN: src = l->attn_o; n = (size_t)c.n_heads * c.head_dim; break;
+    case FASTTPS_DBG_H1: src = l->h1; n = (size_t)c.hidden; break;
+    case FASTTPS_DBG_MLP_A: src = l->mlp_a; n = (size_t)c.intermediate; break;
+    default: return fail(FASTTPS_ERR_INVALID_ARG, "unknown debug buffer %d", which);
+  }
+  n *= (size_t)batch * sizeof(float);
+  if (bytes != n) return fail(FASTTPS_ERR_INVALID_ARG, "bytes %zu != %zu", bytes, n);
+  hipError_t e = hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "debug copy");
+  return FASTTPS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+// Host-side launchers of the gfx950 kernels (internal to libfasttps).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fasttps {
+
+constexpr int kMaxBatch = 64;
+
+struct PosArray {
+  int32_t p[kMaxBatch];
+};
+
+// y[b, r] = sum_c W[r, c] * act[b, c] over `rows` rows of a bf16 [rows, din] matrix.
+struct GemvArgs {
+  const uint16_t* w;       // [rows, din] bf16
+  int rows, din, batch;
+  const uint16_t* x_bf16;  // norm mode: token x [batch, din]; residual mode: x [batch, rows]
+  const uint16_t* gamma;   // norm mode: RMSNorm gain [din]
+  const float* in_f32;     // residual mode: activation [batch, din] fp32
+  float* out;              // [batch, rows] fp32
+  float eps;
+};
+
+// RMSNorm1(x) followed by the fused QKV projection (fp32 out, before RoPE).
+hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s);
+// h1 = x + W_o o  (fp32 out).
+hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s);
+
+struct AttnArgs {
+  const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
+  const double* rope_cos;  // [N_max, d/2]
+  const double* rope_sin;  // [N_max, d/2]
+  uint16_t* k_cache;       // [B, H_kv, N_max, d]
+  uint16_t* v_cache;
+  float* part;             // [batch, H, nsplit_cap, d + 2] split partials (m, l, o)
+  unsigned* tickets;       // [batch, H_kv], zero between calls
+  float* o;                // [batch, H d] fp32
+  int batch, n_heads, n_kv_heads, head_dim, max_seq;
+  int split_len, nsplit, nsplit_cap;
+  float scale;             // 1/sqrt(d)
+  PosArray pos;
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+struct MlpArgs {
+  const float* h1;         // [batch, D] fp32
+  const uint16_t* gamma;   // RMSNorm2 gain [D]
+  const uint16_t* w_gu;    // [2K, D] interlaced in tiles of `tk` rows
+  const uint16_t* w_downT; // [K, D]
+  float* partial;          // [nblk, batch, D] fp32
+  float* a_dbg;            // [batch, K] or null
+  int batch, hidden, inter, tk;
+  float eps;
+};
+hipError_t launch_mlp(const MlpArgs& a, hipStream_t s);
+int mlp_blocks(int inter, int tk);
+
+// y[b, c] = bf16(h1[b, c] + sum_blk partial[blk, b, c])
+hipError_t launch_mlp_reduce(const float* h1, const float* partial, int nblk, int batch, int hidden,
+                             uint16_t* y, hipStream_t s);
+
+// packing (cold path)
+hipError_t launch_interlace_gate_up(const uint16_t* gate, const uint16_t* up, uint16_t* dst, int inter,
+                                    int hidden, int tk, hipStream_t s);
+hipError_t launch_transpose_bf16(const uint16_t* src, uint16_t* dst, int rows, int cols, hipStream_t s);
+
+}  // namespace fasttps

@@ -44,7 +44,11 @@ def fp32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     Inputs here are finite draws, so no NaN/Inf handling is needed.
     """
     u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
-    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    r = u >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
     return r.astype(np.uint16)
 
 

@@ -1,0 +1,185 @@
+"""ctypes binding of libfasttps.so (the C ABI in include/fasttps.h).
+
+Argument marshalling only: every step of the decode layer runs in the HIP
+kernels of the library. Device memory and streams come from PyTorch tensors
+and streams. Importing this module loads the library and raises if it is
+missing; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libfasttps.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_UNSUPPORTED = -2
+ERR_ALIGNMENT = -3
+ERR_CACHE_FULL = -4
+ERR_OOM = -5
+ERR_HIP = -6
+ERR_BAD_HANDLE = -7
+
+DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
+
+EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
+           "fasttps_set_debug", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string",
+           "fasttps_last_error")
+
+
+class FastTPSError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({status_string(status)}): {detail}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("intermediate", ctypes.c_int32), ("max_batch", ctypes.c_int32),
+                ("max_seq", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+
+
+WEIGHT_FIELDS = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm", "w_gate", "w_up", "w_down")
+
+
+class WeightsDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_11211_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.fasttps_layer_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]
+    lib.fasttps_weights_pack.argtypes = [vp, ctypes.POINTER(WeightsDesc), vp, ctypes.POINTER(vp)]
+    lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
+    lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
+    lib.fasttps_set_debug.argtypes = [vp, i32]
+    lib.fasttps_weights_free.argtypes = [vp]
+    lib.fasttps_layer_destroy.argtypes = [vp]
+    lib.fasttps_status_string.argtypes = [ctypes.c_int]
+    lib.fasttps_status_string.restype = ctypes.c_char_p
+    lib.fasttps_last_error.argtypes = []
+    lib.fasttps_last_error.restype = ctypes.c_char_p
+    for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
+                 "fasttps_set_debug", "fasttps_weights_free", "fasttps_layer_destroy"):
+        getattr(lib, name).restype = ctypes.c_int
+    return lib
+
+
+LIB = _load()
+
+
+def status_string(status: int) -> str:
+    return LIB.fasttps_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return LIB.fasttps_last_error().decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise FastTPSError(status, where, last_error())
+
+
+def make_config(cfg, max_batch: Optional[int] = None) -> Config:
+    """C config from a shape record (``configs.LayerConfig``)."""
+    return Config(cfg.hidden, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.intermediate,
+                  cfg.batch if max_batch is None else max_batch, cfg.max_seq, float(cfg.rope_base),
+                  float(cfg.rms_eps))
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) or None
+
+
+class Weights:
+    """Packed weights of one layer (owned by the library)."""
+
+    def __init__(self, layer: "Layer", tensors: Dict[str, "object"], stream=None):
+        desc = WeightsDesc(*[_ptr(tensors[n]) for n in WEIGHT_FIELDS])
+        h = ctypes.c_void_p()
+        _check(LIB.fasttps_weights_pack(layer.handle, ctypes.byref(desc), _stream_handle(stream),
+                                        ctypes.byref(h)), "fasttps_weights_pack")
+        self.handle = h
+
+    def free(self) -> None:
+        if self.handle:
+            _check(LIB.fasttps_weights_free(self.handle), "fasttps_weights_free")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class Layer:
+    """A decode-layer handle: config, scratch and RoPE table on the current device."""
+
+    def __init__(self, cfg, max_batch: Optional[int] = None):
+        self.cfg = cfg
+        self.c = make_config(cfg, max_batch)
+        h = ctypes.c_void_p()
+        _check(LIB.fasttps_layer_create(ctypes.byref(self.c), ctypes.byref(h)), "fasttps_layer_create")
+        self.handle = h
+
+    def pack(self, tensors: Dict[str, "object"], stream=None) -> Weights:
+        return Weights(self, tensors, stream)
+
+    def step(self, weights: Weights, x, pos, k_cache, v_cache, y, stream=None) -> None:
+        """Enqueue one decode step. pos: host ints [batch]; tensors: torch device tensors."""
+        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
+        batch = int(p.shape[0])
+        _check(LIB.fasttps_decode_step(self.handle, weights.handle, _ptr(x),
+                                       p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
+                                       _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
+               "fasttps_decode_step")
+
+    def set_debug(self, enable: bool) -> None:
+        _check(LIB.fasttps_set_debug(self.handle, 1 if enable else 0), "fasttps_set_debug")
+
+    def debug_read(self, which: int, batch: int, dst, stream=None) -> None:
+        _check(LIB.fasttps_debug_read(self.handle, int(which), int(batch), _ptr(dst),
+                                      int(dst.numel() * dst.element_size()), _stream_handle(stream)),
+               "fasttps_debug_read")
+
+    def destroy(self) -> None:
+        if self.handle:
+            _check(LIB.fasttps_layer_destroy(self.handle), "fasttps_layer_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def to_device(bits: np.ndarray, device="cuda"):
+    """Upload bf16 bit patterns (uint16) as an int16 device tensor (same bytes)."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(device)
+
+
+def from_device(t) -> np.ndarray:
+    """Download an int16/bf16 device tensor as uint16 bit patterns."""
+    import torch
+    if t.dtype == torch.bfloat16:
+        t = t.view(torch.int16)
+    return t.cpu().numpy().view(np.uint16)

@@ -1,0 +1,139 @@
+"""Helpers of the GPU parity tests: run the HIP layer through the C ABI and
+compare it with the fp64 oracle on the same seeded inputs."""
+from __future__ import annotations
+
+import sys
+import time
+
+import numpy as np
+
+from oracle import ref
+
+Y_RTOL = 2e-2      # |gpu - ref| <= 2e-2 * max(1, |ref|) per output element
+QKV_TOL = 1e-5     # pre-RoPE q, k, v: relative to max |ref| of the sequence
+O_TOL = 1e-4       # attention output: relative to max |ref| of the (sequence, head)
+DELTA_TOL = 1e-3   # h1 - x and the MLP activation a: relative to max |ref|
+
+
+def log(msg: str) -> None:
+    print(f"[gpu-test {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def bf16_ulp(m: np.ndarray) -> np.ndarray:
+    """Spacing of bf16 numbers in the binade of |m| (m > 0)."""
+    e = np.floor(np.log2(np.maximum(m, np.finfo(np.float64).tiny)))
+    return np.ldexp(1.0, (e - 7).astype(np.int64))
+
+
+def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
+    """Distance of bf16 patterns along the number line (+0 and -0 coincide)."""
+    def key(u):
+        u = u.astype(np.int64)
+        mag = u & 0x7FFF
+        return np.where(u & 0x8000, -mag, mag)
+    return np.abs(key(a_bits) - key(b_bits))
+
+
+def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False):
+    """One decode step on cuda:0 through the C ABI. Returns host copies."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    lay = layer if layer is not None else L.Layer(cfg)
+    W = weights
+    if W is None:
+        wt = {k: L.to_device(v) for k, v in inp.weights.items()}
+        W = lay.pack(wt)
+        del wt
+    x = L.to_device(inp.x)
+    kc = L.to_device(inp.k_cache)
+    vc = L.to_device(inp.v_cache)
+    y = torch.empty_like(x)
+    B = cfg.batch
+    lay.set_debug(debug)
+    lay.step(W, x, inp.pos, kc, vc, y)
+    out = {}
+    if debug:
+        dev = x.device
+        bufs = {"qkv": (L.DBG_QKV, cfg.qkv_rows), "o": (L.DBG_ATTN, cfg.q_dim), "h1": (L.DBG_H1, cfg.hidden),
+                "a": (L.DBG_MLP_A, cfg.intermediate)}
+        for name, (which, n) in bufs.items():
+            t = torch.empty(B, n, dtype=torch.float32, device=dev)
+            lay.debug_read(which, B, t)
+            out[name] = t
+    torch.cuda.synchronize()
+    res = {"y": L.from_device(y), "k_cache": L.from_device(kc), "v_cache": L.from_device(vc)}
+    for k, t in out.items():
+        res[k] = t.cpu().numpy().astype(np.float64)
+    if keep:
+        res["_layer"], res["_weights"] = lay, W
+    return res
+
+
+def check_cache(cfg, inp, gpu, r):
+    """Untouched cache bytes are bit-exact; the appended slot is within 1 ulp."""
+    B, G, d = cfg.batch, cfg.n_kv_heads, cfg.head_dim
+    stats = {}
+    for name, orig, exact in (("k", inp.k_cache, r["k_rope"]), ("v", inp.v_cache, r["v"])):
+        got = gpu[f"{name}_cache"]
+        slot = np.empty((B, G, d), dtype=np.uint16)
+        masked = got.copy()
+        for b in range(B):
+            p = int(inp.pos[b])
+            slot[b] = got[b, :, p, :]
+            masked[b, :, p, :] = orig[b, :, p, :]
+        assert np.array_equal(masked, orig), f"{name}-cache bytes outside the appended slots changed"
+        val = ref.bf16_bits_to_f64(slot)
+        assert np.all(np.isfinite(val)), f"appended {name} holds non-finite values"
+        # one bf16 ulp, measured at max(|ref|, rms of the head / 256)
+        rms = np.sqrt(np.mean(exact ** 2, axis=-1, keepdims=True))
+        ulp = bf16_ulp(np.maximum(np.abs(exact), rms / 256.0))
+        err = np.abs(val - exact)
+        bad = err > ulp
+        want_bits = ref.f64_to_bf16_bits(exact)
+        strict = int(np.sum(ulp_distance(slot, want_bits) > 1))
+        exact_match = int(np.sum(slot == want_bits))
+        stats[name] = dict(n=slot.size, bits_equal=exact_match, strict_miss=strict, miss=int(bad.sum()))
+        assert not bad.any(), (f"appended {name}: {int(bad.sum())} of {bad.size} values beyond 1 ulp; "
+                               f"worst err/ulp {float(np.max(err / ulp)):.2f}")
+    return stats
+
+
+def check_y(gpu, r):
+    got = ref.bf16_bits_to_f64(gpu["y"])
+    want = r["y"]
+    assert np.all(np.isfinite(got)), "y holds non-finite values"
+    err = np.abs(got - want)
+    lim = Y_RTOL * np.maximum(1.0, np.abs(want))
+    assert np.all(err <= lim), f"y: max err/limit {float(np.max(err / lim)):.3f}"
+    return float(np.max(err / np.maximum(1.0, np.abs(want))))
+
+
+def check_intermediates(cfg, inp, gpu, r):
+    B, H, G, d = cfg.batch, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    worst = {}
+    qkv_ref = np.concatenate([r["q"].reshape(B, -1), r["k"].reshape(B, -1), r["v"].reshape(B, -1)], axis=1)
+    e = np.abs(gpu["qkv"] - qkv_ref) / np.max(np.abs(qkv_ref), axis=1, keepdims=True)
+    worst["qkv"] = float(e.max())
+    assert e.max() <= QKV_TOL, f"qkv: {e.max():.3g}"
+    o = gpu["o"].reshape(B, H, d)
+    e = np.abs(o - r["o"]) / np.max(np.abs(r["o"]), axis=2, keepdims=True)
+    worst["o"] = float(e.max())
+    assert e.max() <= O_TOL, f"attention o: {e.max():.3g}"
+    x = ref.bf16_bits_to_f64(inp.x)
+    dref = r["h1"] - x
+    e = np.abs(gpu["h1"] - r["h1"]) / np.max(np.abs(dref), axis=1, keepdims=True)
+    worst["h1"] = float(e.max())
+    assert e.max() <= DELTA_TOL, f"h1: {e.max():.3g}"
+    e = np.abs(gpu["a"] - r["a"]) / np.max(np.abs(r["a"]), axis=1, keepdims=True)
+    worst["a"] = float(e.max())
+    assert e.max() <= DELTA_TOL, f"mlp a: {e.max():.3g}"
+    return worst
+
+
+def full_check(cfg, inp, gpu, r, intermediates=True):
+    stats = check_cache(cfg, inp, gpu, r)
+    yerr = check_y(gpu, r)
+    worst = check_intermediates(cfg, inp, gpu, r) if intermediates else {}
+    log(f"{cfg.name}: pos={inp.pos.tolist()[:8]} y_err={yerr:.2e} cache={stats} inter={worst}")
+    return stats, yerr, worst
+

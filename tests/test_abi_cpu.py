@@ -1,0 +1,106 @@
+"""The C-ABI library on the CPU: it loads, exports what the header declares, and
+rejects bad arguments before any HIP call (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fasttps.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2607_11211_amd import build
+    if not os.path.exists(build.LIB):
+        build.build(verbose=False)
+    import paper_2607_11211_amd.layer as layer
+    return layer
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"FASTTPS_API\s+[\w\s\*]+?\b(fasttps_\w+)\s*\(", text)
+
+
+def test_header_declares_the_abi():
+    names = declared_functions()
+    for n in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_weights_free",
+              "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error", "fasttps_debug_read",
+              "fasttps_set_debug"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L.LIB, name), name
+    assert set(declared_functions()) == set(L.EXPORTS)
+
+
+def test_status_strings(L):
+    seen = set()
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+        s = L.status_string(code)
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 8
+    assert L.status_string(-99) == "unknown status"
+
+
+def _cfg(L, **kw):
+    base = dict(hidden=256, n_heads=4, n_kv_heads=4, head_dim=64, intermediate=688, max_batch=1,
+                max_seq=256, rope_base=10000.0, rms_eps=1e-5)
+    base.update(kw)
+    return L.Config(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=80), -2),
+    (dict(hidden=100), -2),
+    (dict(hidden=16384), -2),
+    (dict(n_heads=6, n_kv_heads=2), -2),
+    (dict(n_heads=6, n_kv_heads=4), -2),
+    (dict(intermediate=689), -2),
+    (dict(rms_eps=0.0), -1),
+    (dict(rope_base=float("nan")), -1),
+    (dict(max_batch=65), -1),
+    (dict(max_batch=0), -1),
+    (dict(max_seq=0), -1),
+    (dict(hidden=-8), -1),
+])
+def test_create_rejects_bad_config(L, kw, code):
+    c = _cfg(L, **kw)
+    h = ctypes.c_void_p()
+    assert L.LIB.fasttps_layer_create(ctypes.byref(c), ctypes.byref(h)) == code
+    assert not h.value
+    assert L.last_error()
+
+
+def test_create_null_arguments(L):
+    h = ctypes.c_void_p()
+    assert L.LIB.fasttps_layer_create(None, ctypes.byref(h)) == L.ERR_INVALID_ARG
+    c = _cfg(L)
+    assert L.LIB.fasttps_layer_create(ctypes.byref(c), None) == L.ERR_INVALID_ARG
+
+
+def test_null_handles_are_rejected(L):
+    assert L.LIB.fasttps_layer_destroy(None) == L.ERR_BAD_HANDLE
+    assert L.LIB.fasttps_weights_free(None) == L.ERR_BAD_HANDLE
+    assert L.LIB.fasttps_set_debug(None, 1) == L.ERR_BAD_HANDLE
+    assert L.LIB.fasttps_debug_read(None, 0, 1, None, 0, None) == L.ERR_BAD_HANDLE
+    pos = (ctypes.c_int32 * 1)(0)
+    assert L.LIB.fasttps_decode_step(None, None, None, pos, 1, None, None, None, None) == L.ERR_BAD_HANDLE
+    h = ctypes.c_void_p()
+    assert L.LIB.fasttps_weights_pack(None, None, None, ctypes.byref(h)) == L.ERR_BAD_HANDLE
+    assert "handle" in L.last_error()
+
+
+def test_create_without_gpu_fails_cleanly(L):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    c = _cfg(L)
+    h = ctypes.c_void_p()
+    assert L.LIB.fasttps_layer_create(ctypes.byref(c), ctypes.byref(h)) == L.ERR_HIP
+    assert not h.value
