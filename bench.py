@@ -1,0 +1,301 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the FastTPS layer library on one MI355X.
+
+Workload (default): the Phi-3-mini-shaped 32-layer stack, batch 1, KV length
+4096 per layer, one decode step = 32 layer steps, each layer with its own
+weights and caches (8.9 GB in all, so no layer's data is still in the 256 MB
+Infinity Cache when the step comes back to it). The reported value is the
+decode-step latency of one layer (step time / 32) in microseconds, next to
+the HBM bandwidth it implies over the algorithmic bytes (every weight once
+plus the K/V entries read), the dominant kernel's roofline, and the fp64
+oracle timed on the host cores.
+
+Inputs are synthetic and seeded: layer 0 comes from the shared input
+generator (the bits the oracle sample uses); layers 1..31 are drawn on the
+device with the same distributions. Everything is resident in HBM before the
+timed region starts.
+"""
+from __future__ import annotations
+
+import argparse
+import dataclasses
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "decode-step layer latency (µs) + achieved HBM GB/s vs peak, Phi-3-mini shape"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_bytes(cfg, pos):
+    """Algorithmic HBM bytes per launch of each kernel (weights once, K/V read once)."""
+    D, K, d = cfg.hidden, cfg.intermediate, cfg.head_dim
+    return {
+        "rmsnorm_qkv": 2 * cfg.qkv_rows * D + 2 * D,
+        "attention": cfg.kv_read_bytes(pos),
+        "attn_combine": 0,
+        "oproj_residual": 2 * D * cfg.q_dim,
+        "mlp_fused": 2 * 3 * K * D + 2 * D,
+        "mlp_reduce": 0,
+    }
+
+
+def source_digest(path: str) -> str:
+    with open(path, "rb") as f:
+        return hashlib.sha1(f.read()).hexdigest()
+
+
+def load_traffic(kernel: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the kernel source as it is now; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    try:
+        info = json.load(open(TRAFFIC_FILE))[kernel]
+        src = os.path.join(ROOT, info["source"])
+        if source_digest(src) != info["source_sha1"]:
+            return None
+        return float(info["bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def device_bits(shape, std, mean, gen):
+    import torch
+    t = torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32)
+    if std != 1.0:
+        t.mul_(std)
+    if mean != 0.0:
+        t.add_(mean)
+    return t.to(torch.bfloat16).view(torch.int16)
+
+
+def device_layer(cfg, layer, pos, gen):
+    """Weights and caches of one layer drawn on the device (same recipe as inputs.py)."""
+    import torch
+    from paper_2607_11211_amd import inputs
+    D, K, q, kv = cfg.hidden, cfg.intermediate, cfg.q_dim, cfg.kv_dim
+    w = {
+        "attn_norm": device_bits((D,), 0.1, 1.0, gen), "w_q": device_bits((q, D), 0.02, 0.0, gen),
+        "w_k": device_bits((kv, D), 0.02, 0.0, gen), "w_v": device_bits((kv, D), 0.02, 0.0, gen),
+        "w_o": device_bits((D, q), 0.02, 0.0, gen), "mlp_norm": device_bits((D,), 0.1, 1.0, gen),
+        "w_gate": device_bits((K, D), 0.02, 0.0, gen), "w_up": device_bits((K, D), 0.02, 0.0, gen),
+        "w_down": device_bits((D, K), 0.02, 0.0, gen),
+    }
+    caches = []
+    for sentinel in (inputs.K_SENTINEL, inputs.V_SENTINEL):
+        c = torch.full((cfg.batch, cfg.n_kv_heads, cfg.max_seq, cfg.head_dim),
+                       int(np.uint16(sentinel).view(np.int16)), dtype=torch.int16, device="cuda")
+        for b in range(cfg.batch):
+            p = int(pos[b])
+            c[b, :, :p].copy_(device_bits((cfg.n_kv_heads, p, cfg.head_dim), 1.0, 0.0, gen))
+        caches.append(c)
+    return w, caches[0], caches[1]
+
+
+def cpu_baseline(cfg, seconds: float):
+    """The fp64 oracle on a bounded sample: layer 0 of the workload, repeated."""
+    from oracle import ref
+    from paper_2607_11211_amd import inputs
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max(blas) if blas else 1
+    except Exception:
+        threads = 1
+    cores = min(threads, len(os.sched_getaffinity(0)))
+    inp = inputs.make_layer_inputs(cfg, layer=0)
+    W = ref.widen_weights(inp.weights)   # outside the timer
+    ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, W)  # warm
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, W)
+        reps += 1
+        el = time.perf_counter() - t0
+        if (el >= seconds and reps >= 3) or reps >= 100000:
+            break
+    us = el / reps * 1e6
+    return {"value": round(us, 1), "unit": "us", "cores": int(cores), "kind": "oracle",
+            "sample": f"one layer ({cfg.name} shape, layer 0 inputs), {reps} repetitions in {el:.1f} s, "
+                      f"fp64 numpy, BLAS threads {threads}",
+            "gbps": round(cfg.step_bytes() / us * 1e-3, 2)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="phi3_stack32_kv4k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs one decode layer on one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding plan is described in DESIGN.md, not implemented)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2607_11211_amd import configs, inputs
+    from paper_2607_11211_amd import layer as L
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    cfg = configs.get(args.workload)
+    nl = cfg.layers
+    pos = inputs.make_pos(cfg)
+    cfg = cfg.with_pos(pos)
+    log(f"workload {cfg.name}: {nl} layers, batch {cfg.batch}, pos {pos.tolist()[:4]}")
+
+    lay = L.Layer(cfg)
+    weights, kcs, vcs = [], [], []
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0xFA57 + cfg.index)
+    host0 = inputs.make_layer_inputs(cfg, layer=0, pos=pos)
+    for li in range(nl):
+        if li == 0:
+            w = {k: L.to_device(v) for k, v in host0.weights.items()}
+            kc, vc = L.to_device(host0.k_cache), L.to_device(host0.v_cache)
+        else:
+            w, kc, vc = device_layer(cfg, li, pos, gen)
+        weights.append(lay.pack(w))
+        del w
+        kcs.append(kc)
+        vcs.append(vc)
+    x0 = L.to_device(host0.x)
+    ys = [torch.empty_like(x0) for _ in range(nl)]
+    torch.cuda.synchronize()
+    log(f"resident: {torch.cuda.memory_allocated() / 2**30:.2f} GiB via torch + packed weights")
+
+    stream = torch.cuda.current_stream()
+
+    def step():
+        x = x0
+        for li in range(nl):
+            lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], stream)
+            x = ys[li]
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    y_ref = L.from_device(ys[-1])
+
+    # timed region: K decode steps on the stream
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    e1.synchronize()
+    stream_ms = e0.elapsed_time(e1) / args.steps
+    log(f"stream: {stream_ms:.3f} ms/step, {stream_ms * 1e3 / nl:.2f} us/layer")
+
+    # per-kernel durations (events stamped from each kernel's dispatch)
+    nprof = min(args.steps, 20) * nl
+    lay.profile_begin(nprof)
+    for _ in range(min(args.steps, 20)):
+        step()
+    kms = lay.profile_end(nprof)
+    names = L.kernel_names()
+    kern_us = {n: float(np.mean(kms[:, i]) * 1e3) for i, n in enumerate(names)}
+    log("kernels (us): " + ", ".join(f"{n} {v:.2f}" for n, v in kern_us.items()))
+
+    # HIP-graph replay of the whole decode step
+    graph_ms = None
+    if not args.no_graph:
+        try:
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(stream)
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    x = x0
+                    for li in range(nl):
+                        lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], s)
+                        x = ys[li]
+            stream.wait_stream(s)
+            torch.cuda.synchronize()
+            ok = True
+            for _ in range(3):  # replays must match the eager result
+                g.replay()
+                torch.cuda.synchronize()
+                ok &= bool(np.array_equal(L.from_device(ys[-1]), y_ref))
+                step()
+                torch.cuda.synchronize()
+            if not ok:
+                log("graph replay disagrees with eager steps; graph timing dropped")
+            else:
+                for _ in range(args.warmup):
+                    g.replay()
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for _ in range(args.steps):
+                    g.replay()
+                e1.record(stream)
+                e1.synchronize()
+                graph_ms = e0.elapsed_time(e1) / args.steps
+                log(f"graph: {graph_ms:.3f} ms/step, {graph_ms * 1e3 / nl:.2f} us/layer")
+        except Exception as ex:  # capture unsupported: report stream timing only
+            log(f"graph capture failed: {ex!r}")
+            graph_ms = None
+
+    ms_step = min(stream_ms, graph_ms) if graph_ms is not None else stream_ms
+    us_layer = ms_step * 1e3 / nl
+    step_bytes = cfg.step_bytes(pos)
+    gbps = step_bytes / (us_layer * 1e-6) / 1e9
+
+    kb = kernel_bytes(cfg, pos)
+    dominant = max(kern_us, key=kern_us.get)
+    ach = kb[dominant] / (kern_us[dominant] * 1e-6) / 1e9 if kb[dominant] else None
+    traffic = load_traffic(dominant)
+    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1) if ach else None,
+                "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBPS, 4) if ach else None,
+                "traffic": traffic, "algorithmic_bytes": kb[dominant],
+                "avg_launch_us": round(kern_us[dominant], 3)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline: timing the fp64 oracle on one layer")
+        one = dataclasses.replace(cfg, layers=1)
+        cpu = cpu_baseline(one, args.cpu_seconds)
+        log(f"cpu baseline: {cpu['value']} us/layer on {cpu['cores']} threads")
+
+    out = {
+        "metric": METRIC, "value": round(us_layer, 3), "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: Phi-3-mini-shaped decoder stack, {nl} layers, batch {cfg.batch}, "
+                               f"KV length {int(pos[0])} per layer, one decode step",
+                   "layers": nl, "global_batch": cfg.batch, "seq_len": int(pos.max()) + 1,
+                   "parallelism": "single GPU"},
+        "hbm_gbps": round(gbps, 1), "hbm_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
+        "bytes_per_layer_step": step_bytes,
+        "us_per_layer_stream": round(stream_ms * 1e3 / nl, 3),
+        "us_per_layer_graph": round(graph_ms * 1e3 / nl, 3) if graph_ms is not None else None,
+        "kernels_us": {k: round(v, 3) for k, v in kern_us.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -142,6 +142,19 @@ FASTTPS_API int fasttps_debug_read(fasttps_layer* layer, int32_t which, int32_t 
 /* Test hook: when enabled, steps also store the MLP intermediate a. */
 FASTTPS_API int fasttps_set_debug(fasttps_layer* layer, int32_t enable);
 
+/* Measurement hook: time every kernel of the next `max_steps` steps of this
+ * handle. Each kernel of those steps is launched with start/stop events that
+ * the runtime stamps from the kernel's own dispatch (no extra stream work).
+ * fasttps_profile_end waits for the last recorded step, writes the kernel
+ * durations in milliseconds to ms[step * FASTTPS_NUM_KERNELS + k] for the
+ * n_steps recorded steps (at most max_steps), and releases the events.
+ * Kernel k is named by fasttps_kernel_name(k). Steps beyond max_steps run
+ * untimed. Not for use under stream capture. */
+#define FASTTPS_NUM_KERNELS 6
+FASTTPS_API int fasttps_profile_begin(fasttps_layer* layer, int32_t max_steps);
+FASTTPS_API int fasttps_profile_end(fasttps_layer* layer, float* ms, int32_t max_steps, int32_t* n_steps);
+FASTTPS_API const char* fasttps_kernel_name(int32_t k);
+
 FASTTPS_API int fasttps_weights_free(fasttps_weights* w);
 FASTTPS_API int fasttps_layer_destroy(fasttps_layer* layer);
 

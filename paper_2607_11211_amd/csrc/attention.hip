@@ -8,19 +8,24 @@
 //   [s*L, s*L + L) of one (b, g) for all G = H/H_kv query heads of that KV
 //   head, so each K/V byte is read from HBM once (grouped-query attention).
 // Per block:
+//   * the loads of the first two K/V tiles are issued before anything else
+//     (the cache does not depend on this step's projections);
 //   * prologue: RoPE on the G query heads and on k, with shared cos/sin rows
 //     in double precision (Alg. 3 joint RoPE; Eq. 22); the block that owns the
 //     new position N_p rounds k and v to bf16 and writes them to slot N_p
 //     (GKVC, Eq. 1). It uses the rounded values straight from LDS; slot N_p
 //     is never read back from memory and no other block touches it;
-//   * K/V tiles of 64 positions are copied to LDS with 16-byte coalesced loads
-//     (each tile is one contiguous range of the [N_max, d] row of (b, g));
+//   * K/V tiles of 64 positions go global -> registers -> LDS with 16-byte
+//     coalesced loads (a tile is one contiguous range of the [N_max, d] row
+//     of (b, g)); the loads of the next two tiles are in flight in registers
+//     while the current tile is computed from LDS;
 //   * four lanes share a position (a quarter of d each): QK^T partials are
 //     finished with two butterflies, and each lane keeps an online-softmax
 //     state (m, l, o-quarter) per query head;
-//   * the block merges its lanes' states, writes (m, l, o) for its split, and
-//     the last split of (b, g) to finish (atomic ticket) combines the splits
-//     with the log-sum-exp identity and writes o. It resets its ticket.
+//   * the block merges its lanes' states and writes (m, l, o) for its split.
+// A second small kernel combines the splits of each (b, head) with the
+// log-sum-exp identity. (Cross-block tickets are avoided on purpose: on this
+// chip an agent-scope fence per block costs far more than a kernel boundary.)
 #include "common.h"
 #include "kernels.h"
 
@@ -31,12 +36,12 @@ namespace fasttps {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTile = 64;        // positions per LDS tile
-constexpr int kMaxSplits = 256;  // bound on splits per (b, g)
+constexpr int kTile = 64;         // positions per LDS tile
+constexpr int kMaxSplits = 256;   // splits per (sequence, kv head); one combine thread each
 
 template <int D, int G>
 struct alignas(16) AttnSmem {
-  uint16_t kt[kTile][D + 8];   // padded rows: 16 extra bytes shift the banks
+  uint16_t kt[kTile][D + 8];  // padded rows: 16 extra bytes shift the banks
   uint16_t vt[kTile][D + 8];
   float q[G][D];
   uint16_t knew[D];
@@ -44,20 +49,113 @@ struct alignas(16) AttnSmem {
   float wm[4][G];
   float wl[4][G];
   float wo[4][G][D];
-  float fac[G][kMaxSplits];
-  float lsum[G];
-  int last;
 };
 
 __device__ __forceinline__ float merge_factor(float m, float M) {
   return (m == -INFINITY) ? 0.f : __expf(m - M);
 }
 
+// Global -> registers: this thread's 16-byte chunks of the tile at t0.
+// Only rows below P hold cached entries (commit keeps only those); the loads
+// themselves are unconditional, with the row clamped into [t0, end), so the
+// staging arrays stay in registers and every load stays in flight until its
+// data is committed.
+template <int D, int NPF>
+__device__ __forceinline__ void tile_issue(v4u (&pk)[NPF], v4u (&pv)[NPF], const v4u* __restrict__ Kc,
+                                           const v4u* __restrict__ Vc, int t0, int end, int tid) {
+  constexpr int C8 = D / 8;
+  const int last = min(kTile, end - t0) - 1;  // >= 0 since t0 < end
+#pragma unroll
+  for (int i = 0; i < NPF; ++i) {
+    const int f = tid + kThreads * i;
+    const int row = min(f / C8, last), c = f % C8;
+    const size_t src = (size_t)(t0 + row) * C8 + c;
+    pk[i] = Kc[src];
+    pv[i] = Vc[src];
+  }
+}
+
+// Registers -> LDS; the new entry (position P, if in this tile) comes from
+// the rounded k/v already in LDS.
+template <int D, int G, int NPF>
+__device__ __forceinline__ void tile_commit(AttnSmem<D, G>& sm, const v4u (&pk)[NPF], const v4u (&pv)[NPF],
+                                            int t0, int end, int P, int tid) {
+  constexpr int C8 = D / 8;
+  const int nvalid = min(kTile, end - t0);
+  const int ncached = max(0, min(nvalid, P - t0));
+#pragma unroll
+  for (int i = 0; i < NPF; ++i) {
+    const int f = tid + kThreads * i;
+    const int row = f / C8, c = f % C8;
+    if (row < ncached) {
+      *reinterpret_cast<v4u*>(&sm.kt[row][c * 8]) = pk[i];
+      *reinterpret_cast<v4u*>(&sm.vt[row][c * 8]) = pv[i];
+    }
+  }
+  if (P >= t0 && P < t0 + nvalid && tid < 2 * C8) {
+    const bool isv = tid >= C8;
+    const int c = isv ? tid - C8 : tid;
+    const v4u val = reinterpret_cast<const v4u*>(isv ? sm.vnew : sm.knew)[c];
+    *reinterpret_cast<v4u*>(isv ? &sm.vt[P - t0][c * 8] : &sm.kt[P - t0][c * 8]) = val;
+  }
+}
+
+// One tile: QK^T for the G query heads, online softmax, PV, for the
+// position j = tid / 4 and the quarter seg = tid % 4 of d this lane owns.
+template <int D, int G>
+__device__ __forceinline__ void tile_compute(const AttnSmem<D, G>& sm, float (&m)[G], float (&l)[G],
+                                             float (&o)[G][D / 4], int nvalid, int j, int seg, float scale) {
+  constexpr int SEG = D / 4;
+  const bool valid = j < nvalid;
+  float sc[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) sc[h] = 0.f;
+  if (valid) {
+    const v4u* kr = reinterpret_cast<const v4u*>(&sm.kt[j][seg * SEG]);
+#pragma unroll
+    for (int c = 0; c < SEG / 8; ++c) {
+      float kf[8];
+      unpack8(kr[c], kf);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float* qh = &sm.q[h][seg * SEG + c * 8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sc[h] = fmaf(qh[e], kf[e], sc[h]);
+      }
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    sc[h] += __shfl_xor(sc[h], 1, kWave);
+    sc[h] += __shfl_xor(sc[h], 2, kWave);
+    sc[h] *= scale;
+  }
+  if (valid) {
+    float vf[SEG];
+    const v4u* vr = reinterpret_cast<const v4u*>(&sm.vt[j][seg * SEG]);
+#pragma unroll
+    for (int c = 0; c < SEG / 8; ++c) unpack8(vr[c], vf + 8 * c);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float mn = fmaxf(m[h], sc[h]);
+      const float cf = merge_factor(m[h], mn);
+      const float p = __expf(sc[h] - mn);
+      l[h] = fmaf(l[h], cf, p);
+#pragma unroll
+      for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, p * vf[e]);
+      m[h] = mn;
+    }
+  }
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
-  constexpr int SEG = D / 4;     // elements of a position row per lane
-  constexpr int C8 = D / 8;      // 16-byte chunks per row
+  constexpr int SEG = D / 4;                  // elements of a position row per lane
+  constexpr int C8 = D / 8;                   // 16-byte chunks per row
   constexpr int HALF = D / 2;
+  constexpr int NPF = kTile * C8 / kThreads;  // 16-byte chunks per thread per tile (K and V each)
+  static_assert(SEG % 8 == 0, "a lane's quarter row must be whole 16-byte chunks");
+  static_assert(NPF * kThreads == kTile * C8, "tile must split evenly over the block");
   __shared__ AttnSmem<D, G> sm;
 
   const int tid = threadIdx.x;
@@ -69,6 +167,17 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const int start = s * a.split_len;
   const int end = min(start + a.split_len, ntot);
   const int H = a.n_heads, Hkv = a.n_kv_heads;
+  const size_t head_off = ((size_t)b * Hkv + g) * (size_t)a.max_seq * D;
+  const v4u* Kc = reinterpret_cast<const v4u*>(a.k_cache + head_off);
+  const v4u* Vc = reinterpret_cast<const v4u*>(a.v_cache + head_off);
+
+  // ---- first two tiles' loads, before the prologue -------------------------
+  // Tiles t+1 and t+2 are in flight in registers while tile t is computed.
+  v4u pk0[NPF], pv0[NPF], pk1[NPF], pv1[NPF];
+  if (start < end) tile_issue<D, NPF>(pk0, pv0, Kc, Vc, start, end, tid);
+  if (start + kTile < end) tile_issue<D, NPF>(pk1, pv1, Kc, Vc, start + kTile, end, tid);
+
+  // ---- prologue: RoPE (double), rounding of the new K/V -------------------
   const size_t rowlen = (size_t)(H + 2 * Hkv) * D;
   const float* qkv = a.qkv + (size_t)b * rowlen;
   const float* qg = qkv + (size_t)g * G * D;
@@ -76,10 +185,7 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const float* vg = qkv + (size_t)(H + Hkv) * D + (size_t)g * D;
   const double* cs = a.rope_cos + (size_t)P * HALF;
   const double* sn = a.rope_sin + (size_t)P * HALF;
-  const size_t head_off = ((size_t)b * Hkv + g) * (size_t)a.max_seq * D;
   const bool own_new = (start <= P) && (P < end);
-
-  // ---- prologue: RoPE (double), append of the new K/V --------------------
   for (int i = tid; i < G * HALF; i += kThreads) {
     const int hq = i / HALF, j = i % HALF;
     const double c = cs[j], sv = sn[j];
@@ -97,12 +203,13 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     for (int j = tid; j < D; j += kThreads) sm.vnew[j] = f32_to_bf16(vg[j]);
   }
   __syncthreads();
+  // GKVC append (Eq. 1): the one cache write of the step
   if (own_new && tid < 2 * C8) {
     const bool isv = tid >= C8;
     const int c = isv ? tid - C8 : tid;
-    const uint4 val = reinterpret_cast<const uint4*>(isv ? sm.vnew : sm.knew)[c];
+    const v4u val = reinterpret_cast<const v4u*>(isv ? sm.vnew : sm.knew)[c];
     uint16_t* dst = (isv ? a.v_cache : a.k_cache) + head_off + (size_t)P * D;
-    reinterpret_cast<uint4*>(dst)[c] = val;
+    reinterpret_cast<v4u*>(dst)[c] = val;
   }
 
   // ---- main loop over tiles ------------------------------------------------
@@ -115,67 +222,21 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < SEG; ++e) o[h][e] = 0.f;
   }
-  const uint4* Kc = reinterpret_cast<const uint4*>(a.k_cache + head_off);
-  const uint4* Vc = reinterpret_cast<const uint4*>(a.v_cache + head_off);
 
-  for (int t0 = start; t0 < end; t0 += kTile) {
-    const int nvalid = min(kTile, end - t0);
-    const int ncached = max(0, min(nvalid, P - t0));
-    for (int f = tid; f < ncached * C8; f += kThreads) {
-      const int row = f / C8, c = f % C8;
-      const size_t src = (size_t)(t0 + row) * C8 + c;
-      *reinterpret_cast<uint4*>(&sm.kt[row][c * 8]) = Kc[src];
-      *reinterpret_cast<uint4*>(&sm.vt[row][c * 8]) = Vc[src];
-    }
-    if (P >= t0 && P < t0 + nvalid && tid < 2 * C8) {
-      const bool isv = tid >= C8;
-      const int c = isv ? tid - C8 : tid;
-      const uint4 val = reinterpret_cast<const uint4*>(isv ? sm.vnew : sm.knew)[c];
-      *reinterpret_cast<uint4*>(isv ? &sm.vt[P - t0][c * 8] : &sm.kt[P - t0][c * 8]) = val;
-    }
+  for (int t0 = start; t0 < end; t0 += 2 * kTile) {
+    __syncthreads();  // every lane is done with the previous tile in LDS
+    tile_commit<D, G, NPF>(sm, pk0, pv0, t0, end, P, tid);
     __syncthreads();
-
-    const bool valid = j < nvalid;
-    float sc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) sc[h] = 0.f;
-    if (valid) {
-      const uint4* kr = reinterpret_cast<const uint4*>(&sm.kt[j][seg * SEG]);
-#pragma unroll
-      for (int c = 0; c < SEG / 8; ++c) {
-        float kf[8];
-        unpack8(kr[c], kf);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float* qh = &sm.q[h][seg * SEG + c * 8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) sc[h] = fmaf(qh[e], kf[e], sc[h]);
-        }
-      }
+    if (t0 + 2 * kTile < end) tile_issue<D, NPF>(pk0, pv0, Kc, Vc, t0 + 2 * kTile, end, tid);
+    tile_compute<D, G>(sm, m, l, o, min(kTile, end - t0), j, seg, a.scale);
+    const int t1 = t0 + kTile;
+    if (t1 < end) {
+      __syncthreads();
+      tile_commit<D, G, NPF>(sm, pk1, pv1, t1, end, P, tid);
+      __syncthreads();
+      if (t1 + 2 * kTile < end) tile_issue<D, NPF>(pk1, pv1, Kc, Vc, t1 + 2 * kTile, end, tid);
+      tile_compute<D, G>(sm, m, l, o, min(kTile, end - t1), j, seg, a.scale);
     }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      sc[h] += __shfl_xor(sc[h], 1, kWave);
-      sc[h] += __shfl_xor(sc[h], 2, kWave);
-      sc[h] *= a.scale;
-    }
-    if (valid) {
-      float vf[SEG];
-      const uint4* vr = reinterpret_cast<const uint4*>(&sm.vt[j][seg * SEG]);
-#pragma unroll
-      for (int c = 0; c < SEG / 8; ++c) unpack8(vr[c], vf + 8 * c);
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float mn = fmaxf(m[h], sc[h]);
-        const float cf = merge_factor(m[h], mn);
-        const float p = __expf(sc[h] - mn);
-        l[h] = fmaf(l[h], cf, p);
-#pragma unroll
-        for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, p * vf[e]);
-        m[h] = mn;
-      }
-    }
-    __syncthreads();
   }
 
   // ---- merge the 16 position groups of each wave, then the 4 waves --------
@@ -204,7 +265,6 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   }
   __syncthreads();
 
-  const int nsplit = a.nsplit;
   float* part_b = a.part + (size_t)b * H * a.nsplit_cap * (D + 2);
   for (int i = tid; i < G * D; i += kThreads) {
     const int h = i / D, e = i % D;
@@ -223,67 +283,91 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
       pr[1] = L;
     }
   }
+}
 
-  // ---- last split of (b, g) combines --------------------------------------
-  __threadfence();
+// o[b, h] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s,  M = max_s m_s.
+// One block per (head, sequence); split s's (m, l) is read by thread s, and
+// the o sums are spread over 256 / D thread groups so loads overlap.
+constexpr int kCombineThreads = 256;
+
+template <int D>
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
+                                                                       int nsplit_cap, int n_heads,
+                                                                       float* __restrict__ o) {
+  constexpr int NG = kCombineThreads / D;  // thread groups over the splits
+  __shared__ float fac[kMaxSplits];
+  __shared__ float red[kCombineThreads / kWave];
+  __shared__ float osum[NG][D];
+  const int tid = threadIdx.x;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + 2);
+  const float ms = tid < nsplit ? ph[(size_t)tid * (D + 2)] : -INFINITY;
+  const float ls = tid < nsplit ? ph[(size_t)tid * (D + 2) + 1] : 0.f;
+  // block max of m
+  float M = wave_max(ms);
+  if ((tid & (kWave - 1)) == 0) red[tid / kWave] = M;
   __syncthreads();
-  if (tid == 0) {
-    const unsigned prev = atomicAdd(&a.tickets[b * Hkv + g], 1u);
-    sm.last = (prev == (unsigned)(nsplit - 1));
+  M = red[0];
+  for (int w = 1; w < kCombineThreads / kWave; ++w) M = fmaxf(M, red[w]);
+  const float f = merge_factor(ms, M);
+  if (tid < nsplit) fac[tid] = f;
+  const float L = block_sum(ls * f, red);  // contains the barrier that publishes fac
+  const int grp = tid / D, e = tid % D;
+  if (grp < NG) {
+    float acc = 0.f;
+#pragma unroll 8
+    for (int q = grp; q < nsplit; q += NG) acc = fmaf(ph[(size_t)q * (D + 2) + 2 + e], fac[q], acc);
+    osum[grp][e] = acc;
   }
   __syncthreads();
-  if (!sm.last) return;
-  __threadfence();
-
-  if (tid < G) {
-    const int h = tid;
-    const float* ph = part_b + (size_t)(g * G + h) * a.nsplit_cap * (D + 2);
-    float M = -INFINITY;
-    for (int q = 0; q < nsplit; ++q) M = fmaxf(M, __builtin_nontemporal_load(ph + (size_t)q * (D + 2)));
-    float L = 0.f;
-    for (int q = 0; q < nsplit; ++q) {
-      const float f = merge_factor(__builtin_nontemporal_load(ph + (size_t)q * (D + 2)), M);
-      sm.fac[h][q] = f;
-      L = fmaf(__builtin_nontemporal_load(ph + (size_t)q * (D + 2) + 1), f, L);
-    }
-    sm.lsum[h] = L;
-  }
-  __syncthreads();
-  for (int i = tid; i < G * D; i += kThreads) {
-    const int h = i / D, e = i % D;
-    const float* ph = part_b + (size_t)(g * G + h) * a.nsplit_cap * (D + 2);
+  if (tid < D) {
     float O = 0.f;
-    for (int q = 0; q < nsplit; ++q) O = fmaf(__builtin_nontemporal_load(ph + (size_t)q * (D + 2) + 2 + e), sm.fac[h][q], O);
-    a.o[(size_t)b * H * D + (size_t)(g * G + h) * D + e] = O / sm.lsum[h];
+#pragma unroll
+    for (int g2 = 0; g2 < NG; ++g2) O += osum[g2][tid];
+    o[((size_t)b * n_heads + h) * D + tid] = O / L;
   }
-  if (tid == 0) a.tickets[b * Hkv + g] = 0u;
 }
 
 template <int D, int G>
-hipError_t launch_dg(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
-  hipLaunchKernelGGL((attn_split_kernel<D, G>), grid, dim3(kThreads), 0, s, a);
-  return hipGetLastError();
+  return ext_launch(attn_split_kernel<D, G>, grid, dim3(kThreads), 0, s, ev, a);
 }
 
 template <int D>
-hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   switch (a.n_heads / a.n_kv_heads) {
-    case 1: return launch_dg<D, 1>(a, s);
-    case 2: return launch_dg<D, 2>(a, s);
-    case 4: return launch_dg<D, 4>(a, s);
+    case 1: return launch_dg<D, 1>(a, s, ev);
+    case 2: return launch_dg<D, 2>(a, s, ev);
+    case 4: return launch_dg<D, 4>(a, s, ev);
     default: return hipErrorInvalidValue;
   }
 }
 
+template <int D>
+hipError_t launch_combine_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
+  dim3 grid(a.n_heads, a.batch);
+  return ext_launch(attn_combine_kernel<D>, grid, dim3(kCombineThreads), 0, s, ev, (const float*)a.part, a.nsplit,
+                    a.nsplit_cap, a.n_heads, a.o);
+}
+
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
-  if (a.nsplit < 1 || a.nsplit > kMaxSplits || a.nsplit > a.nsplit_cap) return hipErrorInvalidValue;
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
+  if (a.nsplit < 1 || a.nsplit > a.nsplit_cap || a.nsplit > kMaxSplits) return hipErrorInvalidValue;
   switch (a.head_dim) {
-    case 64: return launch_d<64>(a, s);
-    case 96: return launch_d<96>(a, s);
-    case 128: return launch_d<128>(a, s);
+    case 64: return launch_d<64>(a, s, ev);
+    case 96: return launch_d<96>(a, s, ev);
+    case 128: return launch_d<128>(a, s, ev);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_attention_combine(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
+  switch (a.head_dim) {
+    case 64: return launch_combine_d<64>(a, s, ev);
+    case 96: return launch_combine_d<96>(a, s, ev);
+    case 128: return launch_combine_d<128>(a, s, ev);
     default: return hipErrorInvalidValue;
   }
 }

@@ -8,6 +8,11 @@ namespace fasttps {
 
 constexpr int kWave = 64;
 
+// 16 bytes as a native vector: copies of it are plain vector moves, so
+// staging arrays of it stay in registers (HIP's uint4 struct is copied with
+// memcpy, which can pin such arrays to scratch memory).
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
 // ---- bfloat16 <-> float -------------------------------------------------
 // bf16 is the upper half of a binary32, so widening is a shift.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -59,6 +64,13 @@ __device__ __forceinline__ float fma8(const uint4 w, const float* h, float acc) 
 }
 
 __device__ __forceinline__ void unpack8(const uint4 w, float* f) {
+  f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x);
+  f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
+  f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z);
+  f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
+}
+
+__device__ __forceinline__ void unpack8(const v4u w, float* f) {
   f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x);
   f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
   f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z);

@@ -23,7 +23,7 @@ namespace {
 constexpr uint64_t kLayerMagic = 0x4641535454505331ull;    // "FASTTPS1"
 constexpr uint64_t kWeightsMagic = 0x4641535454505357ull;  // "FASTTPSW"
 constexpr uint64_t kDeadMagic = 0xDEADDEADDEADDEADull;
-constexpr int kTargetAttnBlocks = 1024;  // ~4 blocks per CU on 256 CUs
+constexpr int kTargetAttnBlocks = 768;  // ~3 blocks per CU on 256 CUs
 constexpr int kAttnTile = 64;
 constexpr int kMaxSplits = 256;
 
@@ -67,11 +67,14 @@ struct fasttps_layer {
   double* rope_sin;
   float* qkv;
   float* attn_part;
-  unsigned* tickets;
   float* attn_o;
   float* h1;
   float* mlp_part;
   float* mlp_a;
+  // per-kernel timing (measurement hook)
+  std::vector<hipEvent_t> prof_events;  // [cap][kernel][start, stop]
+  int prof_cap = 0;
+  int prof_n = 0;
 };
 
 struct fasttps_weights {
@@ -144,6 +147,13 @@ bool weights_ok(const fasttps_weights* w) { return live(g_weights, w) && w->magi
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+void release_events(fasttps_layer* l) {
+  for (hipEvent_t e : l->prof_events) (void)hipEventDestroy(e);
+  l->prof_events.clear();
+  l->prof_cap = 0;
+  l->prof_n = 0;
+}
+
 }  // namespace
 
 extern "C" {
@@ -189,19 +199,18 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
     }
   }
 
-  size_t sizes[9] = {
+  size_t sizes[8] = {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
       (size_t)B * c.n_heads * nsplit_cap * (d + 2) * sizeof(float),
-      (size_t)B * c.n_kv_heads * sizeof(unsigned),
       (size_t)B * c.n_heads * d * sizeof(float),
       (size_t)B * c.hidden * sizeof(float),
       (size_t)nblk * B * c.hidden * sizeof(float),
       (size_t)B * c.intermediate * sizeof(float),
   };
-  size_t total = 0, offs[9];
-  for (int i = 0; i < 9; ++i) {
+  size_t total = 0, offs[8];
+  for (int i = 0; i < 8; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -234,16 +243,14 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   l->rope_sin = reinterpret_cast<double*>(base + offs[1]);
   l->qkv = reinterpret_cast<float*>(base + offs[2]);
   l->attn_part = reinterpret_cast<float*>(base + offs[3]);
-  l->tickets = reinterpret_cast<unsigned*>(base + offs[4]);
-  l->attn_o = reinterpret_cast<float*>(base + offs[5]);
-  l->h1 = reinterpret_cast<float*>(base + offs[6]);
-  l->mlp_part = reinterpret_cast<float*>(base + offs[7]);
-  l->mlp_a = reinterpret_cast<float*>(base + offs[8]);
+  l->attn_o = reinterpret_cast<float*>(base + offs[4]);
+  l->h1 = reinterpret_cast<float*>(base + offs[5]);
+  l->mlp_part = reinterpret_cast<float*>(base + offs[6]);
+  l->mlp_a = reinterpret_cast<float*>(base + offs[7]);
 
   if ((e = hipMemcpy(l->rope_cos, cs.data(), sizes[0], hipMemcpyHostToDevice)) != hipSuccess ||
       (e = hipMemcpy(l->rope_sin, sn.data(), sizes[1], hipMemcpyHostToDevice)) != hipSuccess ||
-      (e = hipMemset(l->tickets, 0, sizes[4])) != hipSuccess ||
-      (e = hipMemset(l->mlp_a, 0, sizes[8])) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) {
+      (e = hipMemset(l->mlp_a, 0, sizes[7])) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) {
     (void)hipFree(arena);
     l->magic = kDeadMagic;
     delete l;
@@ -258,10 +265,54 @@ int fasttps_layer_destroy(fasttps_layer* l) {
   g_last_error.clear();
   if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "layer handle is null or already destroyed");
   track(g_layers, l, false);
+  release_events(l);
   l->magic = kDeadMagic;
   hipError_t e = hipFree(l->arena);
   delete l;
   if (e != hipSuccess) return hip_fail(e, "hipFree");
+  return FASTTPS_OK;
+}
+
+const char* fasttps_kernel_name(int32_t k) {
+  static const char* names[FASTTPS_NUM_KERNELS] = {"rmsnorm_qkv", "attention", "attn_combine",
+                                                   "oproj_residual", "mlp_fused", "mlp_reduce"};
+  return (k >= 0 && k < FASTTPS_NUM_KERNELS) ? names[k] : "";
+}
+
+int fasttps_profile_begin(fasttps_layer* l, int32_t max_steps) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (max_steps < 1 || max_steps > (1 << 16)) return fail(FASTTPS_ERR_INVALID_ARG, "max_steps out of range");
+  release_events(l);
+  l->prof_events.resize((size_t)max_steps * FASTTPS_NUM_KERNELS * 2, nullptr);
+  for (auto& ev : l->prof_events) {
+    hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) {
+      ev = nullptr;
+      release_events(l);
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  l->prof_cap = max_steps;
+  l->prof_n = 0;
+  return FASTTPS_OK;
+}
+
+int fasttps_profile_end(fasttps_layer* l, float* ms, int32_t max_steps, int32_t* n_steps) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (!ms || !n_steps) return fail(FASTTPS_ERR_INVALID_ARG, "null output");
+  const int n = std::min(l->prof_n, (int)max_steps);
+  *n_steps = n;
+  hipError_t e = hipSuccess;
+  if (l->prof_n > 0) e = hipEventSynchronize(l->prof_events[((size_t)l->prof_n * FASTTPS_NUM_KERNELS - 1) * 2 + 1]);
+  for (int i = 0; i < n && e == hipSuccess; ++i)
+    for (int k = 0; k < FASTTPS_NUM_KERNELS && e == hipSuccess; ++k) {
+      const size_t j = ((size_t)i * FASTTPS_NUM_KERNELS + k) * 2;
+      e = hipEventElapsedTime(&ms[(size_t)i * FASTTPS_NUM_KERNELS + k], l->prof_events[j], l->prof_events[j + 1]);
+    }
+  release_events(l);
+  if (e != hipSuccess) return hip_fail(e, "kernel timing");
   return FASTTPS_OK;
 }
 
@@ -389,6 +440,15 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   if (dev != l->device) return fail(FASTTPS_ERR_INVALID_ARG, "current device %d is not the layer's device %d", dev, l->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint16_t* xb = static_cast<const uint16_t*>(x);
+  KernelEvents ev[FASTTPS_NUM_KERNELS];
+  const bool timed = l->prof_n < l->prof_cap;
+  if (timed) {
+    for (int k = 0; k < FASTTPS_NUM_KERNELS; ++k) {
+      const size_t i = ((size_t)l->prof_n * FASTTPS_NUM_KERNELS + k) * 2;
+      ev[k].start = l->prof_events[i];
+      ev[k].stop = l->prof_events[i + 1];
+    }
+  }
 
   GemvArgs qa{};
   qa.w = w->w_qkv;
@@ -399,7 +459,7 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   qa.gamma = w->attn_norm;
   qa.out = l->qkv;
   qa.eps = c.rms_eps;
-  if ((e = launch_rmsnorm_qkv(qa, s)) != hipSuccess) return hip_fail(e, "qkv launch");
+  if ((e = launch_rmsnorm_qkv(qa, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
 
   AttnArgs aa{};
   aa.qkv = l->qkv;
@@ -408,7 +468,6 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   aa.k_cache = static_cast<uint16_t*>(k_cache);
   aa.v_cache = static_cast<uint16_t*>(v_cache);
   aa.part = l->attn_part;
-  aa.tickets = l->tickets;
   aa.o = l->attn_o;
   aa.batch = batch;
   aa.n_heads = c.n_heads;
@@ -420,7 +479,8 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   aa.nsplit_cap = l->nsplit_cap;
   aa.scale = (float)(1.0 / std::sqrt((double)d));
   for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
-  if ((e = launch_attention(aa, s)) != hipSuccess) return hip_fail(e, "attention launch");
+  if ((e = launch_attention(aa, s, ev[1])) != hipSuccess) return hip_fail(e, "attention launch");
+  if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
 
   GemvArgs oa{};
   oa.w = w->w_o;
@@ -431,7 +491,7 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   oa.in_f32 = l->attn_o;
   oa.out = l->h1;
   oa.eps = c.rms_eps;
-  if ((e = launch_oproj_residual(oa, s)) != hipSuccess) return hip_fail(e, "o-proj launch");
+  if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
 
   MlpArgs ma{};
   ma.h1 = l->h1;
@@ -445,10 +505,11 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   ma.inter = c.intermediate;
   ma.tk = l->tk;
   ma.eps = c.rms_eps;
-  if ((e = launch_mlp(ma, s)) != hipSuccess) return hip_fail(e, "mlp launch");
-  if ((e = launch_mlp_reduce(l->h1, l->mlp_part, l->nblk_mlp, batch, (int)D, static_cast<uint16_t*>(y), s)) !=
-      hipSuccess)
+  if ((e = launch_mlp(ma, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp launch");
+  if ((e = launch_mlp_reduce(l->h1, l->mlp_part, l->nblk_mlp, batch, (int)D, static_cast<uint16_t*>(y), s,
+                             ev[5])) != hipSuccess)
     return hip_fail(e, "mlp reduce launch");
+  if (timed) ++l->prof_n;
   return FASTTPS_OK;
 }
 

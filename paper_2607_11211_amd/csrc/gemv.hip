@@ -125,34 +125,35 @@ __global__ __launch_bounds__(kThreads) void gemv_rows_kernel(GemvArgs a) {
 }
 
 template <Mode MODE, int BT>
-hipError_t launch_bt(const GemvArgs& a, hipStream_t s, int rpw) {
+hipError_t launch_bt(const GemvArgs& a, hipStream_t s, int rpw, KernelEvents ev) {
   const int nwaves = kThreads / kWave;
   const int rows_per_block = nwaves * rpw;
   dim3 grid((a.rows + rows_per_block - 1) / rows_per_block, (a.batch + BT - 1) / BT);
   const size_t lds = (size_t)BT * a.din * sizeof(float) + 64 * sizeof(float);
-  if (rpw == 1)
-    hipLaunchKernelGGL((gemv_rows_kernel<BT, 1, MODE>), grid, dim3(kThreads), lds, s, a);
-  else
-    hipLaunchKernelGGL((gemv_rows_kernel<BT, 2, MODE>), grid, dim3(kThreads), lds, s, a);
-  return hipGetLastError();
+  if (rpw == 1) return ext_launch(gemv_rows_kernel<BT, 1, MODE>, grid, dim3(kThreads), lds, s, ev, a);
+  return ext_launch(gemv_rows_kernel<BT, 2, MODE>, grid, dim3(kThreads), lds, s, ev, a);
 }
 
 template <Mode MODE>
-hipError_t launch_mode(const GemvArgs& a, hipStream_t s) {
+hipError_t launch_mode(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
   // batch tile: as many sequences as fit 64 KB of fp32 activations in LDS
   const int cap = (int)((65536 - 256) / ((size_t)a.din * sizeof(float)));
   const int want = a.batch < cap ? a.batch : cap;
   // two rows per wave when that still gives the chip >= 2 blocks per CU
   const int rpw = (a.rows / (4 * 2)) >= 512 ? 2 : 1;
-  if (want >= 8) return launch_bt<MODE, 8>(a, s, rpw);
-  if (want >= 4) return launch_bt<MODE, 4>(a, s, rpw);
-  if (want >= 2) return launch_bt<MODE, 2>(a, s, rpw);
-  return launch_bt<MODE, 1>(a, s, rpw);
+  if (want >= 8) return launch_bt<MODE, 8>(a, s, rpw, ev);
+  if (want >= 4) return launch_bt<MODE, 4>(a, s, rpw, ev);
+  if (want >= 2) return launch_bt<MODE, 2>(a, s, rpw, ev);
+  return launch_bt<MODE, 1>(a, s, rpw, ev);
 }
 
 }  // namespace
 
-hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s) { return launch_mode<Mode::kNormQkv>(a, s); }
-hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s) { return launch_mode<Mode::kResidual>(a, s); }
+hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
+  return launch_mode<Mode::kNormQkv>(a, s, ev);
+}
+hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
+  return launch_mode<Mode::kResidual>(a, s, ev);
+}
 
 }  // namespace fasttps

@@ -1,12 +1,29 @@
 // Host-side launchers of the gfx950 kernels (internal to libfasttps).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace fasttps {
 
 constexpr int kMaxBatch = 64;
+
+// Optional start/stop events of one launch (null: plain launch). They are
+// set from the dispatch packet itself, so timing adds nothing to the stream.
+struct KernelEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
+template <typename... Params, typename... Args>
+inline hipError_t ext_launch(void (*kernel)(Params...), dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                             KernelEvents ev, Args... args) {
+  static_assert(sizeof...(Params) == sizeof...(Args), "argument count");
+  void* argv[] = {static_cast<void*>(&args)...};
+  return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, lds, s, ev.start, ev.stop,
+                            0);
+}
 
 struct PosArray {
   int32_t p[kMaxBatch];
@@ -24,9 +41,9 @@ struct GemvArgs {
 };
 
 // RMSNorm1(x) followed by the fused QKV projection (fp32 out, before RoPE).
-hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s);
+hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 // h1 = x + W_o o  (fp32 out).
-hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s);
+hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
 struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
@@ -35,14 +52,16 @@ struct AttnArgs {
   uint16_t* k_cache;       // [B, H_kv, N_max, d]
   uint16_t* v_cache;
   float* part;             // [batch, H, nsplit_cap, d + 2] split partials (m, l, o)
-  unsigned* tickets;       // [batch, H_kv], zero between calls
   float* o;                // [batch, H d] fp32
   int batch, n_heads, n_kv_heads, head_dim, max_seq;
   int split_len, nsplit, nsplit_cap;
   float scale;             // 1/sqrt(d)
   PosArray pos;
 };
-hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+// per split: RoPE, append, partial softmax state (m, l, o)
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
+// combine the split partials into o
+hipError_t launch_attention_combine(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
 
 struct MlpArgs {
   const float* h1;         // [batch, D] fp32
@@ -54,12 +73,12 @@ struct MlpArgs {
   int batch, hidden, inter, tk;
   float eps;
 };
-hipError_t launch_mlp(const MlpArgs& a, hipStream_t s);
+hipError_t launch_mlp(const MlpArgs& a, hipStream_t s, KernelEvents ev = {});
 int mlp_blocks(int inter, int tk);
 
 // y[b, c] = bf16(h1[b, c] + sum_blk partial[blk, b, c])
 hipError_t launch_mlp_reduce(const float* h1, const float* partial, int nblk, int batch, int hidden,
-                             uint16_t* y, hipStream_t s);
+                             uint16_t* y, hipStream_t s, KernelEvents ev = {});
 
 // packing (cold path)
 hipError_t launch_interlace_gate_up(const uint16_t* gate, const uint16_t* up, uint16_t* dst, int inter,

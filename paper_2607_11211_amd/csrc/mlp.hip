@@ -188,11 +188,10 @@ __global__ __launch_bounds__(kThreads) void mlp_fused_kernel(MlpArgs a) {
 }
 
 template <int BT>
-hipError_t launch_bt(const MlpArgs& a, hipStream_t s) {
+hipError_t launch_bt(const MlpArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(mlp_blocks(a.inter, a.tk), (a.batch + BT - 1) / BT);
   const size_t lds = ((size_t)BT * a.hidden + (size_t)BT * 2 * a.tk + 16) * sizeof(float);
-  hipLaunchKernelGGL((mlp_fused_kernel<BT>), grid, dim3(kThreads), lds, s, a);
-  return hipGetLastError();
+  return ext_launch(mlp_fused_kernel<BT>, grid, dim3(kThreads), lds, s, ev, a);
 }
 
 // Partial sums: block = 64 slices x 4 column quads (16 columns); slice s adds
@@ -238,24 +237,23 @@ __global__ __launch_bounds__(256) void mlp_reduce_kernel(const float* __restrict
 
 int mlp_blocks(int inter, int tk) { return (inter + tk - 1) / tk; }
 
-hipError_t launch_mlp(const MlpArgs& a, hipStream_t s) {
+hipError_t launch_mlp(const MlpArgs& a, hipStream_t s, KernelEvents ev) {
   // batch tile: h2 of BT sequences in LDS, at most 96 KB
   const size_t per = ((size_t)a.hidden + 2 * (size_t)a.tk) * sizeof(float);
   const int cap = (int)((96 * 1024) / per);
   const int want = a.batch < cap ? a.batch : cap;
-  if (want >= 8) return launch_bt<8>(a, s);
-  if (want >= 4) return launch_bt<4>(a, s);
-  if (want >= 2) return launch_bt<2>(a, s);
-  return launch_bt<1>(a, s);
+  if (want >= 8) return launch_bt<8>(a, s, ev);
+  if (want >= 4) return launch_bt<4>(a, s, ev);
+  if (want >= 2) return launch_bt<2>(a, s, ev);
+  return launch_bt<1>(a, s, ev);
 }
 
 hipError_t launch_mlp_reduce(const float* h1, const float* partial, int nblk, int batch, int hidden,
-                             uint16_t* y, hipStream_t s) {
+                             uint16_t* y, hipStream_t s, KernelEvents ev) {
   const int total = batch * hidden;  // multiple of 8
   const int n4 = total / 4;
   dim3 grid((n4 + 3) / 4);
-  hipLaunchKernelGGL(mlp_reduce_kernel, grid, dim3(256), 0, s, h1, partial, nblk, total, y);
-  return hipGetLastError();
+  return ext_launch(mlp_reduce_kernel, grid, dim3(256), 0, s, ev, h1, partial, nblk, total, y);
 }
 
 }  // namespace fasttps

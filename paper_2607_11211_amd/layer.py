@@ -28,8 +28,9 @@ ERR_BAD_HANDLE = -7
 DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
 
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
-           "fasttps_set_debug", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string",
-           "fasttps_last_error")
+           "fasttps_set_debug", "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
+           "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
+NUM_KERNELS = 6
 
 
 class FastTPSError(RuntimeError):
@@ -61,6 +62,10 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_set_debug.argtypes = [vp, i32]
+    lib.fasttps_profile_begin.argtypes = [vp, i32]
+    lib.fasttps_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
+    lib.fasttps_kernel_name.argtypes = [i32]
+    lib.fasttps_kernel_name.restype = ctypes.c_char_p
     lib.fasttps_weights_free.argtypes = [vp]
     lib.fasttps_layer_destroy.argtypes = [vp]
     lib.fasttps_status_string.argtypes = [ctypes.c_int]
@@ -68,7 +73,8 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_last_error.argtypes = []
     lib.fasttps_last_error.restype = ctypes.c_char_p
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
-                 "fasttps_set_debug", "fasttps_weights_free", "fasttps_layer_destroy"):
+                 "fasttps_set_debug", "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
+                 "fasttps_layer_destroy"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -159,6 +165,17 @@ class Layer:
                                       int(dst.numel() * dst.element_size()), _stream_handle(stream)),
                "fasttps_debug_read")
 
+    def profile_begin(self, max_steps: int) -> None:
+        _check(LIB.fasttps_profile_begin(self.handle, int(max_steps)), "fasttps_profile_begin")
+
+    def profile_end(self, max_steps: int) -> np.ndarray:
+        """Per-kernel milliseconds [n_steps, NUM_KERNELS] of the recorded steps."""
+        ms = np.zeros((max_steps, NUM_KERNELS), dtype=np.float32)
+        n = ctypes.c_int32(0)
+        _check(LIB.fasttps_profile_end(self.handle, ms.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                       int(max_steps), ctypes.byref(n)), "fasttps_profile_end")
+        return ms[: n.value]
+
     def destroy(self) -> None:
         if self.handle:
             _check(LIB.fasttps_layer_destroy(self.handle), "fasttps_layer_destroy")
@@ -169,6 +186,10 @@ class Layer:
             self.destroy()
         except Exception:
             pass
+
+
+def kernel_names():
+    return [LIB.fasttps_kernel_name(k).decode() for k in range(NUM_KERNELS)]
 
 
 def to_device(bits: np.ndarray, device="cuda"):
