@@ -171,13 +171,9 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const v4u* Kc = reinterpret_cast<const v4u*>(a.k_cache + head_off);
   const v4u* Vc = reinterpret_cast<const v4u*>(a.v_cache + head_off);
 
-  // ---- first two tiles' loads, before the prologue -------------------------
-  // Tiles t+1 and t+2 are in flight in registers while tile t is computed.
-  v4u pk0[NPF], pv0[NPF], pk1[NPF], pv1[NPF];
-  if (start < end) tile_issue<D, NPF>(pk0, pv0, Kc, Vc, start, end, tid);
-  if (start + kTile < end) tile_issue<D, NPF>(pk1, pv1, Kc, Vc, start + kTile, end, tid);
-
-  // ---- prologue: RoPE (double), rounding of the new K/V -------------------
+  // ---- prologue operands first --------------------------------------------
+  // Vector-memory loads retire in order: the few loads the prologue needs go
+  // out before the tile stream, so waiting for them does not wait for tiles.
   const size_t rowlen = (size_t)(H + 2 * Hkv) * D;
   const float* qkv = a.qkv + (size_t)b * rowlen;
   const float* qg = qkv + (size_t)g * G * D;
@@ -186,22 +182,42 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const double* cs = a.rope_cos + (size_t)P * HALF;
   const double* sn = a.rope_sin + (size_t)P * HALF;
   const bool own_new = (start <= P) && (P < end);
-  for (int i = tid; i < G * HALF; i += kThreads) {
-    const int hq = i / HALF, j = i % HALF;
-    const double c = cs[j], sv = sn[j];
-    const double x0 = qg[hq * D + j], x1 = qg[hq * D + j + HALF];
-    sm.q[hq][j] = (float)(x0 * c - x1 * sv);
-    sm.q[hq][j + HALF] = (float)(x1 * c + x0 * sv);
+  static_assert(G * HALF <= kThreads && D <= kThreads, "one prologue element per thread");
+  const bool has_q = tid < G * HALF;
+  const int pj = tid % HALF;
+  double c_j = 0.0, s_j = 0.0;
+  float q0 = 0.f, q1 = 0.f, k0 = 0.f, k1 = 0.f, v0 = 0.f;
+  if (has_q) {
+    c_j = cs[pj];
+    s_j = sn[pj];
+    q0 = qg[(tid / HALF) * D + pj];
+    q1 = qg[(tid / HALF) * D + pj + HALF];
   }
   if (own_new) {
-    for (int j = tid; j < HALF; j += kThreads) {
-      const double c = cs[j], sv = sn[j];
-      const double k0 = kg[j], k1 = kg[j + HALF];
-      sm.knew[j] = f64_to_bf16(k0 * c - k1 * sv);
-      sm.knew[j + HALF] = f64_to_bf16(k1 * c + k0 * sv);
+    if (tid < HALF) {
+      k0 = kg[tid];
+      k1 = kg[tid + HALF];
     }
-    for (int j = tid; j < D; j += kThreads) sm.vnew[j] = f32_to_bf16(vg[j]);
+    if (tid < D) v0 = vg[tid];
   }
+
+  // ---- first two tiles' loads --------------------------------------------
+  // Tiles t+1 and t+2 are in flight in registers while tile t is computed.
+  v4u pk0[NPF], pv0[NPF], pk1[NPF], pv1[NPF];
+  if (start < end) tile_issue<D, NPF>(pk0, pv0, Kc, Vc, start, end, tid);
+  if (start + kTile < end) tile_issue<D, NPF>(pk1, pv1, Kc, Vc, start + kTile, end, tid);
+
+  // ---- prologue: RoPE in double, rounding of the new K/V ------------------
+  if (has_q) {
+    const int hq = tid / HALF;
+    sm.q[hq][pj] = (float)((double)q0 * c_j - (double)q1 * s_j);
+    sm.q[hq][pj + HALF] = (float)((double)q1 * c_j + (double)q0 * s_j);
+    if (own_new && tid < HALF) {
+      sm.knew[pj] = f64_to_bf16((double)k0 * c_j - (double)k1 * s_j);
+      sm.knew[pj + HALF] = f64_to_bf16((double)k1 * c_j + (double)k0 * s_j);
+    }
+  }
+  if (own_new && tid < D) sm.vnew[tid] = f32_to_bf16(v0);
   __syncthreads();
   // GKVC append (Eq. 1): the one cache write of the step
   if (own_new && tid < 2 * C8) {
@@ -286,9 +302,12 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 }
 
 // o[b, h] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s,  M = max_s m_s.
-// One block per (head, sequence); split s's (m, l) is read by thread s, and
-// the o sums are spread over 256 / D thread groups so loads overlap.
+// One block per (head, sequence). Every load is issued up front (the o rows
+// do not depend on M), so the kernel costs one round trip: thread s reads
+// split s's (m, l); thread (group, e) reads o_s[e] of the splits
+// s = group, group + NG, ...
 constexpr int kCombineThreads = 256;
+constexpr int kCombineRegs = 16;  // splits per thread held in registers
 
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
@@ -301,22 +320,33 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
   const int tid = threadIdx.x;
   const int h = blockIdx.x, b = blockIdx.y;
   const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + 2);
+  const int grp = tid / D, e = tid % D;
+  float ov[kCombineRegs];
+#pragma unroll
+  for (int k = 0; k < kCombineRegs; ++k) {
+    const int q = grp + NG * k;
+    ov[k] = (grp < NG && q < nsplit) ? ph[(size_t)q * (D + 2) + 2 + e] : 0.f;
+  }
   const float ms = tid < nsplit ? ph[(size_t)tid * (D + 2)] : -INFINITY;
   const float ls = tid < nsplit ? ph[(size_t)tid * (D + 2) + 1] : 0.f;
-  // block max of m
   float M = wave_max(ms);
   if ((tid & (kWave - 1)) == 0) red[tid / kWave] = M;
   __syncthreads();
   M = red[0];
+#pragma unroll
   for (int w = 1; w < kCombineThreads / kWave; ++w) M = fmaxf(M, red[w]);
   const float f = merge_factor(ms, M);
   if (tid < nsplit) fac[tid] = f;
-  const float L = block_sum(ls * f, red);  // contains the barrier that publishes fac
-  const int grp = tid / D, e = tid % D;
+  const float L = block_sum(ls * f, red);  // its barriers also publish fac
   if (grp < NG) {
     float acc = 0.f;
-#pragma unroll 8
-    for (int q = grp; q < nsplit; q += NG) acc = fmaf(ph[(size_t)q * (D + 2) + 2 + e], fac[q], acc);
+#pragma unroll
+    for (int k = 0; k < kCombineRegs; ++k) {
+      const int q = grp + NG * k;
+      if (q < nsplit) acc = fmaf(ov[k], fac[q], acc);
+    }
+    for (int q = grp + NG * kCombineRegs; q < nsplit; q += NG)
+      acc = fmaf(ph[(size_t)q * (D + 2) + 2 + e], fac[q], acc);
     osum[grp][e] = acc;
   }
   __syncthreads();

@@ -72,6 +72,7 @@ struct MlpArgs {
   float* a_dbg;            // [batch, K] or null
   int batch, hidden, inter, tk;
   float eps;
+  int lds_rows;            // W_down^T slab rows staged in LDS (set by the launcher)
 };
 hipError_t launch_mlp(const MlpArgs& a, hipStream_t s, KernelEvents ev = {});
 int mlp_blocks(int inter, int tk);
