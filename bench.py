@@ -143,6 +143,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="finish with a plain 256 MiB device copy (reference point for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs one decode layer on one GPU; --gpus {args.gpus} is not supported "
@@ -293,6 +295,15 @@ def main() -> int:
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if args.calibrate_copy:
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE counters
+        # (256 MiB each way) scale the counters read for the layer kernels
+        src = torch.empty(64 << 20, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = src.numel() * 4
     print(json.dumps(out), flush=True)
     return 0
 
