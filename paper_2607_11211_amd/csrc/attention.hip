@@ -8,8 +8,8 @@
 //   [s*L, s*L + L) of one (b, g) for all G = H/H_kv query heads of that KV
 //   head, so each K/V byte is read from HBM once (grouped-query attention).
 // Per block:
-//   * the loads of the first two K/V tiles are issued before anything else
-//     (the cache does not depend on this step's projections);
+//   * the K/V tile loads are issued right after the few prologue loads (the
+//     cache does not depend on this step's projections);
 //   * prologue: RoPE on the G query heads and on k, with shared cos/sin rows
 //     in double precision (Alg. 3 joint RoPE; Eq. 22); the block that owns the
 //     new position N_p rounds k and v to bf16 and writes them to slot N_p
@@ -17,12 +17,13 @@
 //     is never read back from memory and no other block touches it;
 //   * K/V tiles of 64 positions go global -> registers -> LDS with 16-byte
 //     coalesced loads (a tile is one contiguous range of the [N_max, d] row
-//     of (b, g)); the loads of the next two tiles are in flight in registers
-//     while the current tile is computed from LDS;
+//     of (b, g)); a ring of up to three tiles is in flight in registers while
+//     the current tile is computed from LDS;
 //   * four lanes share a position (a quarter of d each): QK^T partials are
-//     finished with two butterflies, and each lane keeps an online-softmax
-//     state (m, l, o-quarter) per query head;
-//   * the block merges its lanes' states and writes (m, l, o) for its split.
+//     finished with two in-quad DPP moves, and each lane keeps an
+//     online-softmax state (m, l, o-quarter) per query head;
+//   * the block merges its lanes' states (DPP within each 16-lane row, then
+//     the 16 rows through LDS) and writes (m, l, o) for its split.
 // A second small kernel combines the splits of each (b, head) with the
 // log-sum-exp identity. (Cross-block tickets are avoided on purpose: on this
 // chip an agent-scope fence per block costs far more than a kernel boundary.)
@@ -39,16 +40,22 @@ constexpr int kThreads = 256;
 constexpr int kTile = 64;         // positions per LDS tile
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head); one combine thread each
 
+constexpr int kRows = kThreads / 16;  // 16-lane DPP rows per block (4 positions each)
+
 template <int D, int G>
 struct alignas(16) AttnSmem {
-  uint16_t kt[kTile][D + 8];  // padded rows: 16 extra bytes shift the banks
-  uint16_t vt[kTile][D + 8];
+  union {
+    struct {
+      uint16_t k[kTile][D + 8];  // padded rows: 16 extra bytes shift the banks
+      uint16_t v[kTile][D + 8];
+    } tile;
+    float red[G][kRows][D];  // after the last tile: the rows' o sums
+  };
   float q[G][D];
   uint16_t knew[D];
   uint16_t vnew[D];
-  float wm[4][G];
-  float wl[4][G];
-  float wo[4][G][D];
+  float rm[G][kRows];  // the rows' running max and sum
+  float rl[G][kRows];
 };
 
 __device__ __forceinline__ float merge_factor(float m, float M) {
@@ -88,15 +95,15 @@ __device__ __forceinline__ void tile_commit(AttnSmem<D, G>& sm, const v4u (&pk)[
     const int f = tid + kThreads * i;
     const int row = f / C8, c = f % C8;
     if (row < ncached) {
-      *reinterpret_cast<v4u*>(&sm.kt[row][c * 8]) = pk[i];
-      *reinterpret_cast<v4u*>(&sm.vt[row][c * 8]) = pv[i];
+      *reinterpret_cast<v4u*>(&sm.tile.k[row][c * 8]) = pk[i];
+      *reinterpret_cast<v4u*>(&sm.tile.v[row][c * 8]) = pv[i];
     }
   }
   if (P >= t0 && P < t0 + nvalid && tid < 2 * C8) {
     const bool isv = tid >= C8;
     const int c = isv ? tid - C8 : tid;
     const v4u val = reinterpret_cast<const v4u*>(isv ? sm.vnew : sm.knew)[c];
-    *reinterpret_cast<v4u*>(isv ? &sm.vt[P - t0][c * 8] : &sm.kt[P - t0][c * 8]) = val;
+    *reinterpret_cast<v4u*>(isv ? &sm.tile.v[P - t0][c * 8] : &sm.tile.k[P - t0][c * 8]) = val;
   }
 }
 
@@ -111,7 +118,7 @@ __device__ __forceinline__ void tile_compute(const AttnSmem<D, G>& sm, float (&m
 #pragma unroll
   for (int h = 0; h < G; ++h) sc[h] = 0.f;
   if (valid) {
-    const v4u* kr = reinterpret_cast<const v4u*>(&sm.kt[j][seg * SEG]);
+    const v4u* kr = reinterpret_cast<const v4u*>(&sm.tile.k[j][seg * SEG]);
 #pragma unroll
     for (int c = 0; c < SEG / 8; ++c) {
       float kf[8];
@@ -125,14 +132,10 @@ __device__ __forceinline__ void tile_compute(const AttnSmem<D, G>& sm, float (&m
     }
   }
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    sc[h] += __shfl_xor(sc[h], 1, kWave);
-    sc[h] += __shfl_xor(sc[h], 2, kWave);
-    sc[h] *= scale;
-  }
+  for (int h = 0; h < G; ++h) sc[h] = quad_sum(sc[h]) * scale;
   if (valid) {
     float vf[SEG];
-    const v4u* vr = reinterpret_cast<const v4u*>(&sm.vt[j][seg * SEG]);
+    const v4u* vr = reinterpret_cast<const v4u*>(&sm.tile.v[j][seg * SEG]);
 #pragma unroll
     for (int c = 0; c < SEG / 8; ++c) unpack8(vr[c], vf + 8 * c);
 #pragma unroll
@@ -148,7 +151,7 @@ __device__ __forceinline__ void tile_compute(const AttnSmem<D, G>& sm, float (&m
   }
 }
 
-template <int D, int G>
+template <int D, int G, int NRING>
 __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   constexpr int SEG = D / 4;                  // elements of a position row per lane
   constexpr int C8 = D / 8;                   // 16-byte chunks per row
@@ -201,11 +204,13 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     if (tid < D) v0 = vg[tid];
   }
 
-  // ---- first two tiles' loads --------------------------------------------
-  // Tiles t+1 and t+2 are in flight in registers while tile t is computed.
-  v4u pk0[NPF], pv0[NPF], pk1[NPF], pv1[NPF];
-  if (start < end) tile_issue<D, NPF>(pk0, pv0, Kc, Vc, start, end, tid);
-  if (start + kTile < end) tile_issue<D, NPF>(pk1, pv1, Kc, Vc, start + kTile, end, tid);
+  // ---- the first NRING tiles' loads ----------------------------------------
+  // A ring of NRING tiles is in flight in registers; a tile's buffer is
+  // refilled with the tile NRING ahead right after it is committed to LDS.
+  v4u pk[NRING][NPF], pv[NRING][NPF];
+#pragma unroll
+  for (int k = 0; k < NRING; ++k)
+    if (start + k * kTile < end) tile_issue<D, NPF>(pk[k], pv[k], Kc, Vc, start + k * kTile, end, tid);
 
   // ---- prologue: RoPE in double, rounding of the new K/V ------------------
   if (has_q) {
@@ -239,44 +244,42 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     for (int e = 0; e < SEG; ++e) o[h][e] = 0.f;
   }
 
-  for (int t0 = start; t0 < end; t0 += 2 * kTile) {
-    __syncthreads();  // every lane is done with the previous tile in LDS
-    tile_commit<D, G, NPF>(sm, pk0, pv0, t0, end, P, tid);
-    __syncthreads();
-    if (t0 + 2 * kTile < end) tile_issue<D, NPF>(pk0, pv0, Kc, Vc, t0 + 2 * kTile, end, tid);
-    tile_compute<D, G>(sm, m, l, o, min(kTile, end - t0), j, seg, a.scale);
-    const int t1 = t0 + kTile;
-    if (t1 < end) {
-      __syncthreads();
-      tile_commit<D, G, NPF>(sm, pk1, pv1, t1, end, P, tid);
-      __syncthreads();
-      if (t1 + 2 * kTile < end) tile_issue<D, NPF>(pk1, pv1, Kc, Vc, t1 + 2 * kTile, end, tid);
-      tile_compute<D, G>(sm, m, l, o, min(kTile, end - t1), j, seg, a.scale);
+  for (int t0 = start; t0 < end; t0 += NRING * kTile) {
+#pragma unroll
+    for (int k = 0; k < NRING; ++k) {
+      const int tt = t0 + k * kTile;
+      if (tt < end) {
+        __syncthreads();  // every lane is done with the previous tile in LDS
+        tile_commit<D, G, NPF>(sm, pk[k], pv[k], tt, end, P, tid);
+        __syncthreads();
+        if (tt + NRING * kTile < end) tile_issue<D, NPF>(pk[k], pv[k], Kc, Vc, tt + NRING * kTile, end, tid);
+        tile_compute<D, G>(sm, m, l, o, min(kTile, end - tt), j, seg, a.scale);
+      }
     }
   }
 
-  // ---- merge the 16 position groups of each wave, then the 4 waves --------
+  // ---- merge: the 4 positions of each 16-lane row (DPP), then the rows ----
+  static_assert(sizeof(float) * G * kRows * D <= sizeof(sm.tile), "merge space fits in the tile buffers");
+  __syncthreads();  // every lane is done with the last tile: its LDS becomes merge space
+  const int row = tid >> 4;
+  const bool row_lead = (tid & 15) < 4;  // lane seg of position 0 of the row
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    float M = m[h];
-    M = fmaxf(M, __shfl_xor(M, 4, kWave));
-    M = fmaxf(M, __shfl_xor(M, 8, kWave));
-    M = fmaxf(M, __shfl_xor(M, 16, kWave));
-    M = fmaxf(M, __shfl_xor(M, 32, kWave));
-    const float f = merge_factor(m[h], M);
-    float lv = l[h] * f;
+    const float Mr = row_stride4_max(m[h]);
+    const float f = merge_factor(m[h], Mr);
+    const float lr = row_stride4_sum(l[h] * f);
 #pragma unroll
-    for (int msk = 4; msk < kWave; msk <<= 1) lv += __shfl_xor(lv, msk, kWave);
+    for (int e = 0; e < SEG; ++e) o[h][e] = row_stride4_sum(o[h][e] * f);
+    if (row_lead) {
+      v4u* dst = reinterpret_cast<v4u*>(&sm.red[h][row][seg * SEG]);
 #pragma unroll
-    for (int e = 0; e < SEG; ++e) {
-      float ov = o[h][e] * f;
-#pragma unroll
-      for (int msk = 4; msk < kWave; msk <<= 1) ov += __shfl_xor(ov, msk, kWave);
-      if (lane < 4) sm.wo[wave][h][lane * SEG + e] = ov;
+      for (int c = 0; c < SEG / 4; ++c)
+        dst[c] = v4u{__float_as_uint(o[h][4 * c]), __float_as_uint(o[h][4 * c + 1]), __float_as_uint(o[h][4 * c + 2]),
+                     __float_as_uint(o[h][4 * c + 3])};
     }
-    if (lane == 0) {
-      sm.wm[wave][h] = M;
-      sm.wl[wave][h] = lv;
+    if ((tid & 15) == 0) {
+      sm.rm[h][row] = Mr;
+      sm.rl[h][row] = lr;
     }
   }
   __syncthreads();
@@ -284,13 +287,15 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   float* part_b = a.part + (size_t)b * H * a.nsplit_cap * (D + 2);
   for (int i = tid; i < G * D; i += kThreads) {
     const int h = i / D, e = i % D;
-    float M = sm.wm[0][h];
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, sm.wm[w][h]);
+    float M = sm.rm[h][0];
+#pragma unroll
+    for (int r = 1; r < kRows; ++r) M = fmaxf(M, sm.rm[h][r]);
     float L = 0.f, O = 0.f;
-    for (int w = 0; w < 4; ++w) {
-      const float f = merge_factor(sm.wm[w][h], M);
-      L = fmaf(sm.wl[w][h], f, L);
-      O = fmaf(sm.wo[w][h][e], f, O);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      const float f = merge_factor(sm.rm[h][r], M);
+      L = fmaf(sm.rl[h][r], f, L);
+      O = fmaf(sm.red[h][r][e], f, O);
     }
     float* pr = part_b + ((size_t)(g * G + h) * a.nsplit_cap + s) * (D + 2);
     pr[2 + e] = O;
@@ -360,8 +365,11 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
 
 template <int D, int G>
 hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
+  // tiles in flight per block: as many as the VGPR budget allows next to
+  // the per-head softmax state (a tile is D / 2 VGPRs of K and V per lane)
+  constexpr int NRING = (G == 1) ? 3 : (G == 2 ? 2 : 1);
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
-  return ext_launch(attn_split_kernel<D, G>, grid, dim3(kThreads), 0, s, ev, a);
+  return ext_launch(attn_split_kernel<D, G, NRING>, grid, dim3(kThreads), 0, s, ev, a);
 }
 
 template <int D>

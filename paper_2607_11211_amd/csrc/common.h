@@ -77,6 +77,36 @@ __device__ __forceinline__ void unpack8(const v4u w, float* f) {
   f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
 }
 
+// ---- data-parallel-primitive (DPP) lane moves ---------------------------
+// Full-rate VALU moves between lanes of a quad (4 lanes) or a row (16
+// lanes); __shfl_xor goes through the LDS crossbar (ds_bpermute) instead.
+constexpr int kDppQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kDppRowRor4 = 0x124;  // rotate right by 4 within each row of 16
+constexpr int kDppRowRor8 = 0x128;  // rotate right by 8 within each row of 16
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 4 lanes of a quad; every lane gets the result.
+__device__ __forceinline__ float quad_sum(float v) {
+  v += dpp_mov<kDppQuadXor1>(v);
+  return v + dpp_mov<kDppQuadXor2>(v);
+}
+
+// Sum / max over the lanes of a 16-lane row that share lane % 4; every lane
+// gets the result for its residue.
+__device__ __forceinline__ float row_stride4_sum(float v) {
+  v += dpp_mov<kDppRowRor4>(v);
+  return v + dpp_mov<kDppRowRor8>(v);
+}
+__device__ __forceinline__ float row_stride4_max(float v) {
+  v = fmaxf(v, dpp_mov<kDppRowRor4>(v));
+  return fmaxf(v, dpp_mov<kDppRowRor8>(v));
+}
+
 // ---- wavefront reductions (64 lanes) ------------------------------------
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
