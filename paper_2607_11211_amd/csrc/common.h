@@ -108,16 +108,33 @@ __device__ __forceinline__ float row_stride4_max(float v) {
 }
 
 // ---- wavefront reductions (64 lanes) ------------------------------------
+// Quad and row steps by DPP, then the row totals are chained with the
+// row_bcast15 / row_bcast31 moves (rows 1 and 3 add the total of the row
+// before; rows 2 and 3 add lane 31), which leaves the wave total in lane 63;
+// a readlane hands it to every lane. The order of the additions is fixed.
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_upd(float old, float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
-  return v;
+  v = row_stride4_sum(quad_sum(v));           // every lane: its row's total
+  v += dpp_upd<kDppRowBcast15, 0xA>(0.f, v);  // rows 1, 3: + previous row
+  v += dpp_upd<kDppRowBcast31, 0xC>(0.f, v);  // rows 2, 3: + rows 0..1
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, kWave));
-  return v;
+  v = fmaxf(v, dpp_mov<kDppQuadXor1>(v));
+  v = fmaxf(v, dpp_mov<kDppQuadXor2>(v));
+  v = row_stride4_max(v);
+  v = fmaxf(v, dpp_upd<kDppRowBcast15, 0xA>(v, v));
+  v = fmaxf(v, dpp_upd<kDppRowBcast31, 0xC>(v, v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 // Sum of x*x over n bf16 values of a row, for the whole block; every thread
