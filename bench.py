@@ -134,6 +134,36 @@ def cpu_baseline(cfg, seconds: float):
             "gbps": round(cfg.step_bytes() / us * 1e-3, 2)}
 
 
+def read_ceiling(nbytes: int = 4 << 30):
+    """Measured HBM read rate in the same run: the stream-read probe (16-byte
+    loads over 4 GiB, 16 times the Infinity Cache) at a few launch shapes,
+    best of three launches each."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_11211_amd", "libfasttps_probe.so"))
+    lib.fasttps_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                                              ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_float)]
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    best = None
+    for blocks in (1024, 2048, 4096, 8192):
+        for unroll in (4, 8):
+            for _ in range(3):
+                ms = ctypes.c_float()
+                rc = lib.fasttps_probe_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                                   ctypes.c_void_p(sink.data_ptr()), blocks, unroll,
+                                                   ctypes.c_void_p(stream), ctypes.byref(ms))
+                if rc != 0:
+                    raise RuntimeError(f"fasttps_probe_stream_read failed: {rc}")
+                gbps = nbytes / (ms.value * 1e-3) / 1e9
+                if best is None or gbps > best[0]:
+                    best = (gbps, blocks, unroll)
+    del buf
+    torch.cuda.empty_cache()
+    return best
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -221,6 +251,7 @@ def main() -> int:
 
     # HIP-graph replay of the whole decode step
     graph_ms = None
+    step_samples = None
     if not args.no_graph:
         try:
             g = torch.cuda.CUDAGraph()
@@ -254,6 +285,15 @@ def main() -> int:
                 e1.synchronize()
                 graph_ms = e0.elapsed_time(e1) / args.steps
                 log(f"graph: {graph_ms:.3f} ms/step, {graph_ms * 1e3 / nl:.2f} us/layer")
+                # the spread over single steps (events around each replay)
+                evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                       for _ in range(args.steps)]
+                for a0, a1 in evs:
+                    a0.record(stream)
+                    g.replay()
+                    a1.record(stream)
+                torch.cuda.synchronize()
+                step_samples = np.array([a0.elapsed_time(a1) for a0, a1 in evs])
         except Exception as ex:  # capture unsupported: report stream timing only
             log(f"graph capture failed: {ex!r}")
             graph_ms = None
@@ -272,6 +312,10 @@ def main() -> int:
                 "traffic": traffic, "algorithmic_bytes": kb[dominant],
                 "avg_launch_us": round(kern_us[dominant], 3)}
 
+    ceiling, c_blocks, c_unroll = read_ceiling()
+    log(f"read ceiling (stream-read probe, 4 GiB): {ceiling:.0f} GB/s at {c_blocks} blocks, unroll {c_unroll}")
+    wbytes = cfg.weight_bytes()
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline: timing the fp64 oracle on one layer")
@@ -288,6 +332,13 @@ def main() -> int:
                    "layers": nl, "global_batch": cfg.batch, "seq_len": int(pos.max()) + 1,
                    "parallelism": "single GPU"},
         "hbm_gbps": round(gbps, 1), "hbm_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
+        "read_ceiling": {"gbps": round(ceiling, 1),
+                         "method": f"libfasttps_probe stream read of 4 GiB with 16-byte loads, best launch "
+                                   f"({c_blocks} blocks x 256 threads, {c_unroll} loads in flight per thread)",
+                         "layer_frac_of_ceiling": round(gbps / ceiling, 4)},
+        "weights_only_gbps": round(wbytes / (us_layer * 1e-6) / 1e9, 1),
+        "us_per_layer_p10_p50_p90": ([round(float(np.percentile(step_samples, q)) * 1e3 / nl, 3)
+                                      for q in (10, 50, 90)] if step_samples is not None else None),
         "bytes_per_layer_step": step_bytes,
         "us_per_layer_stream": round(stream_ms * 1e3 / nl, 3),
         "us_per_layer_graph": round(graph_ms * 1e3 / nl, 3) if graph_ms is not None else None,

@@ -1,4 +1,5 @@
-"""Build libfasttps.so (HIP kernels + C ABI) for gfx950 with hipcc.
+"""Build libfasttps.so (HIP kernels + C ABI) and the measurement aid
+libfasttps_probe.so for gfx950 with hipcc.
 
 Usage: python -m paper_2607_11211_amd.build   (or build() from Python)
 Objects go to paper_2607_11211_amd/_build/, the library next to this file.
@@ -17,8 +18,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfasttps.so")
+PROBE_LIB = os.path.join(PKG, "libfasttps_probe.so")
 
 SOURCES = ["gemv.hip", "attention.hip", "mlp.hip", "pack.hip", "fasttps.cpp"]
+PROBE_SOURCES = ["stream_read.hip"]
 
 ARCH = "gfx950"
 FLAGS = [
@@ -50,18 +53,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = True) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(lib: str, objs) -> None:
+    tmp = lib + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = True) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = dict(zip(srcs, ex.map(_compile, srcs)))
+    _link(LIB, [objs[s] for s in SOURCES])
+    _link(PROBE_LIB, [objs[s] for s in PROBE_SOURCES])
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 

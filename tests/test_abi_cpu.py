@@ -38,6 +38,26 @@ def test_library_exports_every_declared_symbol(L):
     assert set(declared_functions()) == set(L.EXPORTS)
 
 
+def test_probe_library_exports_its_header():
+    """The measurement aid (stream-read probe) is a library of its own with
+    its own header; it rejects bad arguments before touching the GPU."""
+    from paper_2607_11211_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        build.build(verbose=False)
+    text = open(os.path.join(ROOT, "include", "fasttps_probe.h")).read()
+    names = re.findall(r"FASTTPS_PROBE_API\s+[\w\s\*]+?\b(fasttps_\w+)\s*\(", text)
+    assert names == ["fasttps_probe_stream_read"]
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    f = lib.fasttps_probe_stream_read
+    f.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                  ctypes.POINTER(ctypes.c_float)]
+    ms = ctypes.c_float()
+    assert f(None, 16, ctypes.c_void_p(64), 1, 1, None, ctypes.byref(ms)) == -1      # null source
+    assert f(ctypes.c_void_p(64), 24, ctypes.c_void_p(64), 1, 1, None, ctypes.byref(ms)) == -1  # not 16-multiple
+    assert f(ctypes.c_void_p(64), 16, ctypes.c_void_p(64), 1, 3, None, ctypes.byref(ms)) == -1  # unroll 3
+    assert f(ctypes.c_void_p(64), 16, ctypes.c_void_p(64), 0, 1, None, ctypes.byref(ms)) == -1  # no blocks
+
+
 def test_status_strings(L):
     seen = set()
     for code in (0, -1, -2, -3, -4, -5, -6, -7):
