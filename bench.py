@@ -48,8 +48,8 @@ def kernel_bytes(cfg, pos):
         "attention": cfg.kv_read_bytes(pos),
         "attn_combine": 0,
         "oproj_residual": 2 * D * cfg.q_dim,
-        "mlp_fused": 2 * 3 * K * D + 2 * D,
-        "mlp_reduce": 0,
+        "mlp_gate_up": 2 * 2 * K * D + 2 * D,
+        "mlp_down": 2 * K * D,
     }
 
 

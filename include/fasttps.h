@@ -64,7 +64,7 @@ typedef struct {
   int32_t n_heads;       /* H query heads; H / H_kv in {1, 2, 4}; H * d <= 8192 */
   int32_t n_kv_heads;    /* H_kv */
   int32_t head_dim;      /* d in {64, 96, 128} */
-  int32_t intermediate;  /* K (MLP width); multiple of 8, <= 65536 */
+  int32_t intermediate;  /* K (MLP width); multiple of 8, <= 32768 */
   int32_t max_batch;     /* B_max in [1, 64] */
   int32_t max_seq;       /* N_max = N_p + N_r: cache capacity per sequence (Eq. 1), >= 1 */
   float rope_base;       /* RoPE base (e.g. 1e4, 5e5); angle_j(n) = n * base^(-2j/d) */
@@ -93,8 +93,8 @@ FASTTPS_API int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** 
 
 /* Pack one layer's raw weights into the library's layout: fused [W_q; W_k;
  * W_v] rows, interlaced gate/up rows (Section 3.2 item 1, Alg. 4: tiles of
- * gate rows alternate with the matching up rows), and W_down transposed to
- * [K, D] so each MLP block streams its own K-slice. Runs on `stream` and
+ * gate rows alternate with the matching up rows) and W_down as given
+ * ([D, K], one contiguous K-row per output). Runs on `stream` and
  * returns once the copies are complete; the raw weights may then be freed.
  * The packed weights belong to the returned handle (free with
  * fasttps_weights_free) and may be used with any layer handle of the same
@@ -129,8 +129,7 @@ FASTTPS_API int fasttps_decode_step(fasttps_layer* layer, const fasttps_weights*
  *   FASTTPS_DBG_QKV   [batch, (H + 2 H_kv) d]  q | k | v before RoPE
  *   FASTTPS_DBG_ATTN  [batch, H d]             attention output o
  *   FASTTPS_DBG_H1    [batch, D]               x + W_o o
- *   FASTTPS_DBG_MLP_A [batch, K]               SiLU(gate) * up (written only
- *                                               when fasttps_set_debug(layer, 1))
+ *   FASTTPS_DBG_MLP_A [batch, K]               SiLU(gate) * up (h^sm of Alg. 4)
  * `bytes` must equal the size of the selected buffer for `batch`. */
 #define FASTTPS_DBG_QKV   0
 #define FASTTPS_DBG_ATTN  1
@@ -138,9 +137,6 @@ FASTTPS_API int fasttps_decode_step(fasttps_layer* layer, const fasttps_weights*
 #define FASTTPS_DBG_MLP_A 3
 FASTTPS_API int fasttps_debug_read(fasttps_layer* layer, int32_t which, int32_t batch, void* dst,
                        size_t bytes, void* stream);
-
-/* Test hook: when enabled, steps also store the MLP intermediate a. */
-FASTTPS_API int fasttps_set_debug(fasttps_layer* layer, int32_t enable);
 
 /* Measurement hook: time every kernel of the next `max_steps` steps of this
  * handle. Each kernel of those steps is launched with start/stop events that

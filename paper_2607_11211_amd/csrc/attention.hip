@@ -162,8 +162,6 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   __shared__ AttnSmem<D, G> sm;
 
   const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
   const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int P = a.pos.p[b];
   const int ntot = P + 1;

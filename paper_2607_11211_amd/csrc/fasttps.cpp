@@ -61,7 +61,7 @@ struct fasttps_layer {
   uint64_t magic;
   fasttps_config cfg;
   int device;
-  int tk, nblk_mlp, nsplit_cap, debug;
+  int tk, nsplit_cap;
   void* arena;
   double* rope_cos;
   double* rope_sin;
@@ -69,7 +69,6 @@ struct fasttps_layer {
   float* attn_part;
   float* attn_o;
   float* h1;
-  float* mlp_part;
   float* mlp_a;
   // per-kernel timing (measurement hook)
   std::vector<hipEvent_t> prof_events;  // [cap][kernel][start, stop]
@@ -85,7 +84,7 @@ struct fasttps_weights {
   uint16_t* w_qkv;
   uint16_t* w_o;
   uint16_t* w_gu;
-  uint16_t* w_downT;
+  uint16_t* w_down;
   uint16_t* attn_norm;
   uint16_t* mlp_norm;
 };
@@ -112,8 +111,8 @@ int validate_config(const fasttps_config* c) {
     return fail(FASTTPS_ERR_UNSUPPORTED, "n_heads / n_kv_heads = %d: supported 1, 2, 4", group);
   if ((long)c->n_heads * c->head_dim > 8192)
     return fail(FASTTPS_ERR_UNSUPPORTED, "n_heads * head_dim > 8192");
-  if (c->intermediate % 8 != 0 || c->intermediate > 65536)
-    return fail(FASTTPS_ERR_UNSUPPORTED, "intermediate %d: need a multiple of 8 up to 65536", c->intermediate);
+  if (c->intermediate % 8 != 0 || c->intermediate > 32768)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "intermediate %d: need a multiple of 8 up to 32768", c->intermediate);
   if ((long)c->max_seq * c->head_dim * c->n_kv_heads * c->max_batch > (1L << 40))
     return fail(FASTTPS_ERR_UNSUPPORTED, "cache too large");
   return FASTTPS_OK;
@@ -184,7 +183,6 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   const int d = c.head_dim, half = d / 2;
   const int B = c.max_batch;
   const int tk = mlp_tile(c.intermediate);
-  const int nblk = ceil_div(c.intermediate, tk);
   const int nsplit_cap = std::min({kMaxSplits, ceil_div(kTargetAttnBlocks, c.n_kv_heads), ceil_div(c.max_seq, kAttnTile)});
   const size_t qkv_rows = (size_t)(c.n_heads + 2 * c.n_kv_heads) * d;
 
@@ -199,18 +197,17 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
     }
   }
 
-  size_t sizes[8] = {
+  size_t sizes[7] = {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
       (size_t)B * c.n_heads * nsplit_cap * (d + 2) * sizeof(float),
       (size_t)B * c.n_heads * d * sizeof(float),
       (size_t)B * c.hidden * sizeof(float),
-      (size_t)nblk * B * c.hidden * sizeof(float),
       (size_t)B * c.intermediate * sizeof(float),
   };
-  size_t total = 0, offs[8];
-  for (int i = 0; i < 8; ++i) {
+  size_t total = 0, offs[7];
+  for (int i = 0; i < 7; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -235,9 +232,7 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   l->cfg = c;
   l->device = dev;
   l->tk = tk;
-  l->nblk_mlp = nblk;
   l->nsplit_cap = nsplit_cap;
-  l->debug = 0;
   l->arena = arena;
   l->rope_cos = reinterpret_cast<double*>(base + offs[0]);
   l->rope_sin = reinterpret_cast<double*>(base + offs[1]);
@@ -245,12 +240,11 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   l->attn_part = reinterpret_cast<float*>(base + offs[3]);
   l->attn_o = reinterpret_cast<float*>(base + offs[4]);
   l->h1 = reinterpret_cast<float*>(base + offs[5]);
-  l->mlp_part = reinterpret_cast<float*>(base + offs[6]);
-  l->mlp_a = reinterpret_cast<float*>(base + offs[7]);
+  l->mlp_a = reinterpret_cast<float*>(base + offs[6]);
 
   if ((e = hipMemcpy(l->rope_cos, cs.data(), sizes[0], hipMemcpyHostToDevice)) != hipSuccess ||
       (e = hipMemcpy(l->rope_sin, sn.data(), sizes[1], hipMemcpyHostToDevice)) != hipSuccess ||
-      (e = hipMemset(l->mlp_a, 0, sizes[7])) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) {
+      (e = hipMemset(l->mlp_a, 0, sizes[6])) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) {
     (void)hipFree(arena);
     l->magic = kDeadMagic;
     delete l;
@@ -275,7 +269,7 @@ int fasttps_layer_destroy(fasttps_layer* l) {
 
 const char* fasttps_kernel_name(int32_t k) {
   static const char* names[FASTTPS_NUM_KERNELS] = {"rmsnorm_qkv", "attention", "attn_combine",
-                                                   "oproj_residual", "mlp_fused", "mlp_reduce"};
+                                                   "oproj_residual", "mlp_gate_up", "mlp_down"};
   return (k >= 0 && k < FASTTPS_NUM_KERNELS) ? names[k] : "";
 }
 
@@ -316,13 +310,6 @@ int fasttps_profile_end(fasttps_layer* l, float* ms, int32_t max_steps, int32_t*
   return FASTTPS_OK;
 }
 
-int fasttps_set_debug(fasttps_layer* l, int32_t enable) {
-  g_last_error.clear();
-  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
-  l->debug = enable ? 1 : 0;
-  return FASTTPS_OK;
-}
-
 int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* stream, fasttps_weights** out) {
   g_last_error.clear();
   if (!out) return fail(FASTTPS_ERR_INVALID_ARG, "out is null");
@@ -360,7 +347,7 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   pw->w_qkv = reinterpret_cast<uint16_t*>(base + offs[0]);
   pw->w_o = reinterpret_cast<uint16_t*>(base + offs[1]);
   pw->w_gu = reinterpret_cast<uint16_t*>(base + offs[2]);
-  pw->w_downT = reinterpret_cast<uint16_t*>(base + offs[3]);
+  pw->w_down = reinterpret_cast<uint16_t*>(base + offs[3]);
   pw->attn_norm = reinterpret_cast<uint16_t*>(base + offs[4]);
   pw->mlp_norm = reinterpret_cast<uint16_t*>(base + offs[5]);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -373,8 +360,7 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
       (e = hipMemcpyAsync(pw->attn_norm, w->attn_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->mlp_norm, w->mlp_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, l->tk, s)) != hipSuccess ||
-      (e = launch_transpose_bf16(static_cast<const uint16_t*>(w->w_down), pw->w_downT, (int)D, (int)K, s)) !=
-          hipSuccess ||
+      (e = hipMemcpyAsync(pw->w_down, w->w_down, n_d * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = hipStreamSynchronize(s)) != hipSuccess) {
     (void)hipStreamSynchronize(s);
     (void)hipFree(arena);
@@ -497,18 +483,24 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   ma.h1 = l->h1;
   ma.gamma = w->mlp_norm;
   ma.w_gu = w->w_gu;
-  ma.w_downT = w->w_downT;
-  ma.partial = l->mlp_part;
-  ma.a_dbg = l->debug ? l->mlp_a : nullptr;
+  ma.a = l->mlp_a;
   ma.batch = batch;
   ma.hidden = (int)D;
   ma.inter = c.intermediate;
   ma.tk = l->tk;
   ma.eps = c.rms_eps;
-  if ((e = launch_mlp(ma, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp launch");
-  if ((e = launch_mlp_reduce(l->h1, l->mlp_part, l->nblk_mlp, batch, (int)D, static_cast<uint16_t*>(y), s,
-                             ev[5])) != hipSuccess)
-    return hip_fail(e, "mlp reduce launch");
+  if ((e = launch_mlp_gate_up(ma, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
+
+  GemvArgs da{};
+  da.w = w->w_down;
+  da.rows = (int)D;
+  da.din = c.intermediate;
+  da.batch = batch;
+  da.in_f32 = l->mlp_a;
+  da.res_f32 = l->h1;
+  da.out_bf16 = static_cast<uint16_t*>(y);
+  da.eps = c.rms_eps;
+  if ((e = launch_down_residual(da, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
   if (timed) ++l->prof_n;
   return FASTTPS_OK;
 }

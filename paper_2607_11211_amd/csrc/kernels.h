@@ -35,8 +35,10 @@ struct GemvArgs {
   int rows, din, batch;
   const uint16_t* x_bf16;  // norm mode: token x [batch, din]; residual mode: x [batch, rows]
   const uint16_t* gamma;   // norm mode: RMSNorm gain [din]
-  const float* in_f32;     // residual mode: activation [batch, din] fp32
-  float* out;              // [batch, rows] fp32
+  const float* in_f32;     // residual and down modes: activation [batch, din] fp32
+  float* out;              // norm and residual modes: [batch, rows] fp32
+  const float* res_f32;    // down mode: residual h1 [batch, rows] fp32
+  uint16_t* out_bf16;      // down mode: y [batch, rows] bf16
   float eps;
 };
 
@@ -44,6 +46,8 @@ struct GemvArgs {
 hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 // h1 = x + W_o o  (fp32 out).
 hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
+// y = bf16(h1 + W_down a)  (din = K up to 32768).
+hipError_t launch_down_residual(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
 struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
@@ -67,23 +71,16 @@ struct MlpArgs {
   const float* h1;         // [batch, D] fp32
   const uint16_t* gamma;   // RMSNorm2 gain [D]
   const uint16_t* w_gu;    // [2K, D] interlaced in tiles of `tk` rows
-  const uint16_t* w_downT; // [K, D]
-  float* partial;          // [nblk, batch, D] fp32
-  float* a_dbg;            // [batch, K] or null
+  float* a;                // [batch, K] fp32: SiLU(gate) * up
   int batch, hidden, inter, tk;
   float eps;
-  int lds_rows;            // W_down^T slab rows staged in LDS (set by the launcher)
 };
-hipError_t launch_mlp(const MlpArgs& a, hipStream_t s, KernelEvents ev = {});
+// RMSNorm2, interlaced gate/up projection and siLu_Mul -> a
+hipError_t launch_mlp_gate_up(const MlpArgs& a, hipStream_t s, KernelEvents ev = {});
 int mlp_blocks(int inter, int tk);
-
-// y[b, c] = bf16(h1[b, c] + sum_blk partial[blk, b, c])
-hipError_t launch_mlp_reduce(const float* h1, const float* partial, int nblk, int batch, int hidden,
-                             uint16_t* y, hipStream_t s, KernelEvents ev = {});
 
 // packing (cold path)
 hipError_t launch_interlace_gate_up(const uint16_t* gate, const uint16_t* up, uint16_t* dst, int inter,
                                     int hidden, int tk, hipStream_t s);
-hipError_t launch_transpose_bf16(const uint16_t* src, uint16_t* dst, int rows, int cols, hipStream_t s);
 
 }  // namespace fasttps

@@ -46,7 +46,7 @@ extern "C" int fasttps_probe_stream_read(const void* src, size_t bytes, void* si
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (hipEventCreate(&e0) != hipSuccess) return -6;
   if (hipEventCreate(&e1) != hipSuccess) {
-    hipEventDestroy(e0);
+    (void)hipEventDestroy(e0);
     return -6;
   }
   const size_t n = bytes / 16;
@@ -63,7 +63,7 @@ extern "C" int fasttps_probe_stream_read(const void* src, size_t bytes, void* si
   if (err == hipSuccess) err = hipEventRecord(e1, s);
   if (err == hipSuccess) err = hipEventSynchronize(e1);
   if (err == hipSuccess) err = hipEventElapsedTime(ms, e0, e1);
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
   return err == hipSuccess ? 0 : -6;
 }

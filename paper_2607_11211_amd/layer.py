@@ -28,7 +28,7 @@ ERR_BAD_HANDLE = -7
 DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
 
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
-           "fasttps_set_debug", "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
+           "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 6
 
@@ -61,7 +61,6 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_weights_pack.argtypes = [vp, ctypes.POINTER(WeightsDesc), vp, ctypes.POINTER(vp)]
     lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
-    lib.fasttps_set_debug.argtypes = [vp, i32]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
     lib.fasttps_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
     lib.fasttps_kernel_name.argtypes = [i32]
@@ -73,7 +72,7 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_last_error.argtypes = []
     lib.fasttps_last_error.restype = ctypes.c_char_p
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
-                 "fasttps_set_debug", "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
+                 "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
                  "fasttps_layer_destroy"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
@@ -156,9 +155,6 @@ class Layer:
                                        p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
                                        _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step")
-
-    def set_debug(self, enable: bool) -> None:
-        _check(LIB.fasttps_set_debug(self.handle, 1 if enable else 0), "fasttps_set_debug")
 
     def debug_read(self, which: int, batch: int, dst, stream=None) -> None:
         _check(LIB.fasttps_debug_read(self.handle, int(which), int(batch), _ptr(dst),

@@ -49,7 +49,6 @@ def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False):
     vc = L.to_device(inp.v_cache)
     y = torch.empty_like(x)
     B = cfg.batch
-    lay.set_debug(debug)
     lay.step(W, x, inp.pos, kc, vc, y)
     out = {}
     if debug:

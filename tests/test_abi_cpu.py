@@ -28,7 +28,7 @@ def test_header_declares_the_abi():
     names = declared_functions()
     for n in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_weights_free",
               "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error", "fasttps_debug_read",
-              "fasttps_set_debug"):
+              "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name"):
         assert n in names
 
 
@@ -82,6 +82,7 @@ def _cfg(L, **kw):
     (dict(n_heads=6, n_kv_heads=2), -2),
     (dict(n_heads=6, n_kv_heads=4), -2),
     (dict(intermediate=689), -2),
+    (dict(intermediate=32776), -2),
     (dict(rms_eps=0.0), -1),
     (dict(rope_base=float("nan")), -1),
     (dict(max_batch=65), -1),
@@ -107,7 +108,6 @@ def test_create_null_arguments(L):
 def test_null_handles_are_rejected(L):
     assert L.LIB.fasttps_layer_destroy(None) == L.ERR_BAD_HANDLE
     assert L.LIB.fasttps_weights_free(None) == L.ERR_BAD_HANDLE
-    assert L.LIB.fasttps_set_debug(None, 1) == L.ERR_BAD_HANDLE
     assert L.LIB.fasttps_debug_read(None, 0, 1, None, 0, None) == L.ERR_BAD_HANDLE
     pos = (ctypes.c_int32 * 1)(0)
     assert L.LIB.fasttps_decode_step(None, None, None, pos, 1, None, None, None, None) == L.ERR_BAD_HANDLE
