@@ -53,7 +53,10 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 int round_up(int v, int m) { return (v + m - 1) / m * m; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-int mlp_tile(int inter) { return round_up(ceil_div(inter, 256), 8); }
+// Interlaced W_gu (Section 3.2 item 1, Alg. 4) in tiles of one row: packed
+// row 2k is W_gate row k, row 2k + 1 is W_up row k, so the gate/up pair of an
+// intermediate unit is one contiguous 2D-value row for the projection kernel.
+constexpr int kInterlaceTile = 1;
 
 }  // namespace
 
@@ -61,7 +64,7 @@ struct fasttps_layer {
   uint64_t magic;
   fasttps_config cfg;
   int device;
-  int tk, nsplit_cap;
+  int nsplit_cap;
   void* arena;
   double* rope_cos;
   double* rope_sin;
@@ -79,7 +82,6 @@ struct fasttps_layer {
 struct fasttps_weights {
   uint64_t magic;
   fasttps_config cfg;
-  int tk;
   void* arena;
   uint16_t* w_qkv;
   uint16_t* w_o;
@@ -182,7 +184,6 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   const fasttps_config c = *cfg;
   const int d = c.head_dim, half = d / 2;
   const int B = c.max_batch;
-  const int tk = mlp_tile(c.intermediate);
   const int nsplit_cap = std::min({kMaxSplits, ceil_div(kTargetAttnBlocks, c.n_kv_heads), ceil_div(c.max_seq, kAttnTile)});
   const size_t qkv_rows = (size_t)(c.n_heads + 2 * c.n_kv_heads) * d;
 
@@ -231,7 +232,6 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   l->magic = kLayerMagic;
   l->cfg = c;
   l->device = dev;
-  l->tk = tk;
   l->nsplit_cap = nsplit_cap;
   l->arena = arena;
   l->rope_cos = reinterpret_cast<double*>(base + offs[0]);
@@ -342,7 +342,6 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   char* base = static_cast<char*>(arena);
   pw->magic = kWeightsMagic;
   pw->cfg = c;
-  pw->tk = l->tk;
   pw->arena = arena;
   pw->w_qkv = reinterpret_cast<uint16_t*>(base + offs[0]);
   pw->w_o = reinterpret_cast<uint16_t*>(base + offs[1]);
@@ -359,7 +358,7 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
       (e = hipMemcpyAsync(pw->w_o, w->w_o, n_o * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->attn_norm, w->attn_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->mlp_norm, w->mlp_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, l->tk, s)) != hipSuccess ||
+      (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, kInterlaceTile, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->w_down, w->w_down, n_d * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = hipStreamSynchronize(s)) != hipSuccess) {
     (void)hipStreamSynchronize(s);
@@ -390,7 +389,7 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
   if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad weights handle");
   const fasttps_config& c = l->cfg;
-  if (!same_shape(c, w->cfg) || w->tk != l->tk)
+  if (!same_shape(c, w->cfg))
     return fail(FASTTPS_ERR_BAD_HANDLE, "weights were packed for another layer shape");
   if (!x || !pos || !k_cache || !v_cache || !y) return fail(FASTTPS_ERR_INVALID_ARG, "null pointer argument");
   if (batch < 1 || batch > c.max_batch)
@@ -479,17 +478,16 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   oa.eps = c.rms_eps;
   if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
 
-  MlpArgs ma{};
-  ma.h1 = l->h1;
-  ma.gamma = w->mlp_norm;
-  ma.w_gu = w->w_gu;
-  ma.a = l->mlp_a;
-  ma.batch = batch;
-  ma.hidden = (int)D;
-  ma.inter = c.intermediate;
-  ma.tk = l->tk;
-  ma.eps = c.rms_eps;
-  if ((e = launch_mlp_gate_up(ma, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
+  GemvArgs ga{};
+  ga.w = w->w_gu;
+  ga.rows = c.intermediate;
+  ga.din = (int)D;
+  ga.batch = batch;
+  ga.gamma = w->mlp_norm;
+  ga.in_f32 = l->h1;
+  ga.out = l->mlp_a;
+  ga.eps = c.rms_eps;
+  if ((e = launch_gate_up(ga, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
 
   GemvArgs da{};
   da.w = w->w_down;

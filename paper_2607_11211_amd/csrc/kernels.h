@@ -29,16 +29,17 @@ struct PosArray {
   int32_t p[kMaxBatch];
 };
 
-// y[b, r] = sum_c W[r, c] * act[b, c] over `rows` rows of a bf16 [rows, din] matrix.
+// y[b, r] = sum_c W[r, c] * act[b, c] over `rows` rows of a bf16 [rows, din]
+// matrix ([rows, 2 din] for the gate/up pairs).
 struct GemvArgs {
-  const uint16_t* w;       // [rows, din] bf16
+  const uint16_t* w;       // [rows, din] bf16 (gate/up: [rows, 2 din], row k = [gate k | up k])
   int rows, din, batch;
-  const uint16_t* x_bf16;  // norm mode: token x [batch, din]; residual mode: x [batch, rows]
-  const uint16_t* gamma;   // norm mode: RMSNorm gain [din]
-  const float* in_f32;     // residual and down modes: activation [batch, din] fp32
-  float* out;              // norm and residual modes: [batch, rows] fp32
-  const float* res_f32;    // down mode: residual h1 [batch, rows] fp32
-  uint16_t* out_bf16;      // down mode: y [batch, rows] bf16
+  const uint16_t* x_bf16;  // QKV: token x [batch, din]; O proj: residual x [batch, rows]
+  const uint16_t* gamma;   // QKV, gate/up: RMSNorm gain [din]
+  const float* in_f32;     // O proj, down: activation [batch, din]; gate/up: h1 [batch, din] (fp32)
+  float* out;              // QKV, O proj, gate/up: [batch, rows] fp32
+  const float* res_f32;    // down: residual h1 [batch, rows] fp32
+  uint16_t* out_bf16;      // down: y [batch, rows] bf16
   float eps;
 };
 
@@ -48,6 +49,9 @@ hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s, KernelEvents ev 
 hipError_t launch_oproj_residual(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 // y = bf16(h1 + W_down a)  (din = K up to 32768).
 hipError_t launch_down_residual(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
+// a = SiLU(W_gate h2) * (W_up h2), h2 = RMSNorm2(h1), over the interlaced
+// W_gu with tiles of one row (rows = K).
+hipError_t launch_gate_up(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
 struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
@@ -66,18 +70,6 @@ struct AttnArgs {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
 // combine the split partials into o
 hipError_t launch_attention_combine(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
-
-struct MlpArgs {
-  const float* h1;         // [batch, D] fp32
-  const uint16_t* gamma;   // RMSNorm2 gain [D]
-  const uint16_t* w_gu;    // [2K, D] interlaced in tiles of `tk` rows
-  float* a;                // [batch, K] fp32: SiLU(gate) * up
-  int batch, hidden, inter, tk;
-  float eps;
-};
-// RMSNorm2, interlaced gate/up projection and siLu_Mul -> a
-hipError_t launch_mlp_gate_up(const MlpArgs& a, hipStream_t s, KernelEvents ev = {});
-int mlp_blocks(int inter, int tk);
 
 // packing (cold path)
 hipError_t launch_interlace_gate_up(const uint16_t* gate, const uint16_t* up, uint16_t* dst, int inter,
