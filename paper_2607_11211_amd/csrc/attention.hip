@@ -7,21 +7,24 @@
 //   grid = (split, kv head g, sequence b); a block covers positions
 //   [s*L, s*L + L) of one (b, g) for all G = H/H_kv query heads of that KV
 //   head, so each K/V byte is read from HBM once (grouped-query attention).
-// Per block:
-//   * the K/V tile loads are issued right after the few prologue loads (the
-//     cache does not depend on this step's projections);
+// Per block (256 threads, tiles of 64 positions):
+//   * four lanes share a position, each owning a quarter of d: a lane loads
+//     exactly the K and V chunks it computes with (the four lanes of a
+//     position read one contiguous row), straight into registers, with a
+//     ring of NRING tiles in flight. No tile passes through LDS and the loop
+//     has no barrier;
+//   * the prologue's few loads go out first, then the ring: a wave's loads
+//     return in the order they were issued. Every load is issued
+//     unconditionally (rows past the split are clamped into it and masked),
+//     so the compiler waits for exactly the tile it needs;
 //   * prologue: RoPE on the G query heads and on k, with shared cos/sin rows
 //     in double precision (Alg. 3 joint RoPE; Eq. 22); the block that owns the
 //     new position N_p rounds k and v to bf16 and writes them to slot N_p
-//     (GKVC, Eq. 1). It uses the rounded values straight from LDS; slot N_p
-//     is never read back from memory and no other block touches it;
-//   * K/V tiles of 64 positions go global -> registers -> LDS with 16-byte
-//     coalesced loads (a tile is one contiguous range of the [N_max, d] row
-//     of (b, g)); a ring of up to three tiles is in flight in registers while
-//     the current tile is computed from LDS;
-//   * four lanes share a position (a quarter of d each): QK^T partials are
-//     finished with two in-quad DPP moves, and each lane keeps an
-//     online-softmax state (m, l, o-quarter) per query head;
+//     (GKVC, Eq. 1). The lanes of position N_p take the rounded values from
+//     LDS: slot N_p is never read back from memory and no other block
+//     touches it;
+//   * QK^T partials are finished with two in-quad DPP moves, and each lane
+//     keeps an online-softmax state (m, l, o-quarter) per query head;
 //   * the block merges its lanes' states (DPP within each 16-lane row, then
 //     the 16 rows through LDS) and writes (m, l, o) for its split.
 // A second small kernel combines the splits of each (b, head) with the
@@ -37,24 +40,18 @@ namespace fasttps {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTile = 64;         // positions per LDS tile
+constexpr int kTile = 64;         // positions per tile (4 lanes each)
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head); one combine thread each
 
 constexpr int kRows = kThreads / 16;  // 16-lane DPP rows per block (4 positions each)
 
 template <int D, int G>
 struct alignas(16) AttnSmem {
-  union {
-    struct {
-      uint16_t k[kTile][D + 8];  // padded rows: 16 extra bytes shift the banks
-      uint16_t v[kTile][D + 8];
-    } tile;
-    float red[G][kRows][D];  // after the last tile: the rows' o sums
-  };
   float q[G][D];
   uint16_t knew[D];
   uint16_t vnew[D];
-  float rm[G][kRows];  // the rows' running max and sum
+  float red[G][kRows][D];  // the rows' o sums
+  float rm[G][kRows];      // the rows' running max and sum
   float rl[G][kRows];
 };
 
@@ -62,103 +59,27 @@ __device__ __forceinline__ float merge_factor(float m, float M) {
   return (m == -INFINITY) ? 0.f : __expf(m - M);
 }
 
-// Global -> registers: this thread's 16-byte chunks of the tile at t0.
-// Only rows below P hold cached entries (commit keeps only those); the loads
-// themselves are unconditional, with the row clamped into [t0, end), so the
-// staging arrays stay in registers and every load stays in flight until its
-// data is committed.
-template <int D, int NPF>
-__device__ __forceinline__ void tile_issue(v4u (&pk)[NPF], v4u (&pv)[NPF], const v4u* __restrict__ Kc,
-                                           const v4u* __restrict__ Vc, int t0, int end, int tid) {
-  constexpr int C8 = D / 8;
-  const int last = min(kTile, end - t0) - 1;  // >= 0 since t0 < end
+// This lane's K and V chunks of the tile at t0: position t0 + j (clamped to
+// `last`, a position of this split), quarter `seg` of d.
+template <int D>
+__device__ __forceinline__ void tile_load(v4u (&k)[D / 32], v4u (&v)[D / 32], const v4u* __restrict__ Kc,
+                                          const v4u* __restrict__ Vc, int t0, int last, int j, int seg) {
+  constexpr int C8 = D / 8, CH = D / 32;
+  const size_t base = (size_t)min(t0 + j, last) * C8 + seg * CH;
 #pragma unroll
-  for (int i = 0; i < NPF; ++i) {
-    const int f = tid + kThreads * i;
-    const int row = min(f / C8, last), c = f % C8;
-    const size_t src = (size_t)(t0 + row) * C8 + c;
-    pk[i] = Kc[src];
-    pv[i] = Vc[src];
-  }
-}
-
-// Registers -> LDS; the new entry (position P, if in this tile) comes from
-// the rounded k/v already in LDS.
-template <int D, int G, int NPF>
-__device__ __forceinline__ void tile_commit(AttnSmem<D, G>& sm, const v4u (&pk)[NPF], const v4u (&pv)[NPF],
-                                            int t0, int end, int P, int tid) {
-  constexpr int C8 = D / 8;
-  const int nvalid = min(kTile, end - t0);
-  const int ncached = max(0, min(nvalid, P - t0));
-#pragma unroll
-  for (int i = 0; i < NPF; ++i) {
-    const int f = tid + kThreads * i;
-    const int row = f / C8, c = f % C8;
-    if (row < ncached) {
-      *reinterpret_cast<v4u*>(&sm.tile.k[row][c * 8]) = pk[i];
-      *reinterpret_cast<v4u*>(&sm.tile.v[row][c * 8]) = pv[i];
-    }
-  }
-  if (P >= t0 && P < t0 + nvalid && tid < 2 * C8) {
-    const bool isv = tid >= C8;
-    const int c = isv ? tid - C8 : tid;
-    const v4u val = reinterpret_cast<const v4u*>(isv ? sm.vnew : sm.knew)[c];
-    *reinterpret_cast<v4u*>(isv ? &sm.tile.v[P - t0][c * 8] : &sm.tile.k[P - t0][c * 8]) = val;
-  }
-}
-
-// One tile: QK^T for the G query heads, online softmax, PV, for the
-// position j = tid / 4 and the quarter seg = tid % 4 of d this lane owns.
-template <int D, int G>
-__device__ __forceinline__ void tile_compute(const AttnSmem<D, G>& sm, float (&m)[G], float (&l)[G],
-                                             float (&o)[G][D / 4], int nvalid, int j, int seg, float scale) {
-  constexpr int SEG = D / 4;
-  const bool valid = j < nvalid;
-  float sc[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) sc[h] = 0.f;
-  if (valid) {
-    const v4u* kr = reinterpret_cast<const v4u*>(&sm.tile.k[j][seg * SEG]);
-#pragma unroll
-    for (int c = 0; c < SEG / 8; ++c) {
-      float kf[8];
-      unpack8(kr[c], kf);
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float* qh = &sm.q[h][seg * SEG + c * 8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sc[h] = fmaf(qh[e], kf[e], sc[h]);
-      }
-    }
-  }
-#pragma unroll
-  for (int h = 0; h < G; ++h) sc[h] = quad_sum(sc[h]) * scale;
-  if (valid) {
-    float vf[SEG];
-    const v4u* vr = reinterpret_cast<const v4u*>(&sm.tile.v[j][seg * SEG]);
-#pragma unroll
-    for (int c = 0; c < SEG / 8; ++c) unpack8(vr[c], vf + 8 * c);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mn = fmaxf(m[h], sc[h]);
-      const float cf = merge_factor(m[h], mn);
-      const float p = __expf(sc[h] - mn);
-      l[h] = fmaf(l[h], cf, p);
-#pragma unroll
-      for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, p * vf[e]);
-      m[h] = mn;
-    }
+  for (int c = 0; c < CH; ++c) {
+    k[c] = Kc[base + c];
+    v[c] = Vc[base + c];
   }
 }
 
 template <int D, int G, int NRING>
 __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
-  constexpr int SEG = D / 4;                  // elements of a position row per lane
-  constexpr int C8 = D / 8;                   // 16-byte chunks per row
+  constexpr int SEG = D / 4;   // elements of a position row per lane
+  constexpr int CH = D / 32;   // 16-byte chunks per lane (K and V each)
+  constexpr int C8 = D / 8;    // 16-byte chunks per row
   constexpr int HALF = D / 2;
-  constexpr int NPF = kTile * C8 / kThreads;  // 16-byte chunks per thread per tile (K and V each)
   static_assert(SEG % 8 == 0, "a lane's quarter row must be whole 16-byte chunks");
-  static_assert(NPF * kThreads == kTile * C8, "tile must split evenly over the block");
   __shared__ AttnSmem<D, G> sm;
 
   const int tid = threadIdx.x;
@@ -167,14 +88,14 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const int ntot = P + 1;
   const int start = s * a.split_len;
   const int end = min(start + a.split_len, ntot);
+  const int last = max(end - 1, start);  // a cache row of this split (start < N_max)
   const int H = a.n_heads, Hkv = a.n_kv_heads;
   const size_t head_off = ((size_t)b * Hkv + g) * (size_t)a.max_seq * D;
   const v4u* Kc = reinterpret_cast<const v4u*>(a.k_cache + head_off);
   const v4u* Vc = reinterpret_cast<const v4u*>(a.v_cache + head_off);
+  const int j = tid >> 2, seg = tid & 3;
 
-  // ---- prologue operands first --------------------------------------------
-  // Vector-memory loads retire in order: the few loads the prologue needs go
-  // out before the tile stream, so waiting for them does not wait for tiles.
+  // ---- prologue operands first (every thread loads; clamped) ---------------
   const size_t rowlen = (size_t)(H + 2 * Hkv) * D;
   const float* qkv = a.qkv + (size_t)b * rowlen;
   const float* qg = qkv + (size_t)g * G * D;
@@ -184,43 +105,29 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const double* sn = a.rope_sin + (size_t)P * HALF;
   const bool own_new = (start <= P) && (P < end);
   static_assert(G * HALF <= kThreads && D <= kThreads, "one prologue element per thread");
-  const bool has_q = tid < G * HALF;
   const int pj = tid % HALF;
-  double c_j = 0.0, s_j = 0.0;
-  float q0 = 0.f, q1 = 0.f, k0 = 0.f, k1 = 0.f, v0 = 0.f;
-  if (has_q) {
-    c_j = cs[pj];
-    s_j = sn[pj];
-    q0 = qg[(tid / HALF) * D + pj];
-    q1 = qg[(tid / HALF) * D + pj + HALF];
-  }
-  if (own_new) {
-    if (tid < HALF) {
-      k0 = kg[tid];
-      k1 = kg[tid + HALF];
-    }
-    if (tid < D) v0 = vg[tid];
-  }
+  const int ph = min(tid / HALF, G - 1);
+  const double c_j = cs[pj], s_j = sn[pj];
+  const float q0 = qg[ph * D + pj], q1 = qg[ph * D + pj + HALF];
+  const float k0 = kg[pj], k1 = kg[pj + HALF];
+  const float v0 = vg[tid % D];
+  __builtin_amdgcn_sched_barrier(0);  // keep the prologue loads ahead of the tiles
 
-  // ---- the first NRING tiles' loads ----------------------------------------
-  // A ring of NRING tiles is in flight in registers; a tile's buffer is
-  // refilled with the tile NRING ahead right after it is committed to LDS.
-  v4u pk[NRING][NPF], pv[NRING][NPF];
+  // ---- the ring's first NRING tiles ------------------------------------------
+  v4u kr[NRING][CH], vr[NRING][CH];
 #pragma unroll
-  for (int k = 0; k < NRING; ++k)
-    if (start + k * kTile < end) tile_issue<D, NPF>(pk[k], pv[k], Kc, Vc, start + k * kTile, end, tid);
+  for (int r = 0; r < NRING; ++r) tile_load<D>(kr[r], vr[r], Kc, Vc, start + r * kTile, last, j, seg);
 
-  // ---- prologue: RoPE in double, rounding of the new K/V ------------------
-  if (has_q) {
-    const int hq = tid / HALF;
-    sm.q[hq][pj] = (float)((double)q0 * c_j - (double)q1 * s_j);
-    sm.q[hq][pj + HALF] = (float)((double)q1 * c_j + (double)q0 * s_j);
-    if (own_new && tid < HALF) {
-      sm.knew[pj] = f64_to_bf16((double)k0 * c_j - (double)k1 * s_j);
-      sm.knew[pj + HALF] = f64_to_bf16((double)k1 * c_j + (double)k0 * s_j);
-    }
+  // ---- prologue: RoPE in double, rounding of the new K/V --------------------
+  if (tid < G * HALF) {
+    sm.q[ph][pj] = (float)((double)q0 * c_j - (double)q1 * s_j);
+    sm.q[ph][pj + HALF] = (float)((double)q1 * c_j + (double)q0 * s_j);
   }
-  if (own_new && tid < D) sm.vnew[tid] = f32_to_bf16(v0);
+  if (tid < HALF) {
+    sm.knew[pj] = f64_to_bf16((double)k0 * c_j - (double)k1 * s_j);
+    sm.knew[pj + HALF] = f64_to_bf16((double)k1 * c_j + (double)k0 * s_j);
+  }
+  if (tid < D) sm.vnew[tid] = f32_to_bf16(v0);
   __syncthreads();
   // GKVC append (Eq. 1): the one cache write of the step
   if (own_new && tid < 2 * C8) {
@@ -230,9 +137,15 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     uint16_t* dst = (isv ? a.v_cache : a.k_cache) + head_off + (size_t)P * D;
     reinterpret_cast<v4u*>(dst)[c] = val;
   }
+  // this lane's quarter of the query heads: registers for one head, LDS
+  // (read as a broadcast) for a group
+  float qr[G == 1 ? SEG : 1];
+  if (G == 1) {
+#pragma unroll
+    for (int e = 0; e < SEG; ++e) qr[e] = sm.q[0][seg * SEG + e];
+  }
 
-  // ---- main loop over tiles ------------------------------------------------
-  const int j = tid >> 2, seg = tid & 3;
+  // ---- main loop over tiles: the cached entries [start, min(end, P)) ------
   float m[G], l[G], o[G][SEG];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -241,24 +154,58 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < SEG; ++e) o[h][e] = 0.f;
   }
-
-  for (int t0 = start; t0 < end; t0 += NRING * kTile) {
+  const float scale = a.scale;
+  const int cend = min(end, P);  // slot P holds the new entry, handled below
+  // one step of the online softmax with key kf and value vf
+  auto update = [&](const float (&kf)[SEG], const float (&vf)[SEG], bool valid) {
 #pragma unroll
-    for (int k = 0; k < NRING; ++k) {
-      const int tt = t0 + k * kTile;
-      if (tt < end) {
-        __syncthreads();  // every lane is done with the previous tile in LDS
-        tile_commit<D, G, NPF>(sm, pk[k], pv[k], tt, end, P, tid);
-        __syncthreads();
-        if (tt + NRING * kTile < end) tile_issue<D, NPF>(pk[k], pv[k], Kc, Vc, tt + NRING * kTile, end, tid);
-        tile_compute<D, G>(sm, m, l, o, min(kTile, end - tt), j, seg, a.scale);
+    for (int h = 0; h < G; ++h) {
+      float sc = 0.f;
+#pragma unroll
+      for (int e = 0; e < SEG; ++e) sc = fmaf(G == 1 ? qr[e] : sm.q[h][seg * SEG + e], kf[e], sc);
+      sc = quad_sum(sc) * scale;
+      if (valid) {
+        const float mn = fmaxf(m[h], sc);
+        const float cf = merge_factor(m[h], mn);
+        const float p = __expf(sc - mn);
+        l[h] = fmaf(l[h], cf, p);
+#pragma unroll
+        for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, p * vf[e]);
+        m[h] = mn;
       }
     }
+  };
+  for (int t0 = start; t0 < end; t0 += NRING * kTile) {
+#pragma unroll
+    for (int r = 0; r < NRING; ++r) {
+      const int tt = t0 + r * kTile;
+      float kf[SEG], vf[SEG];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        unpack8(kr[r][c], kf + 8 * c);
+        unpack8(vr[r][c], vf + 8 * c);
+      }
+      // refill the slot with the tile NRING further on (clamped past the end);
+      // the barrier keeps the refill after the unpack, so the new tile lands
+      // in the registers the old one leaves (no copies, no early waits)
+      __builtin_amdgcn_sched_barrier(0);
+      tile_load<D>(kr[r], vr[r], Kc, Vc, tt + NRING * kTile, last, j, seg);
+      update(kf, vf, tt + j < cend);
+    }
+  }
+  // the new entry N_p (Eq. 1 slot) from the rounded values in LDS, by the
+  // four lanes of position 0
+  if (own_new && j == 0) {
+    float kf[SEG], vf[SEG];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      unpack8(reinterpret_cast<const v4u*>(sm.knew)[seg * CH + c], kf + 8 * c);
+      unpack8(reinterpret_cast<const v4u*>(sm.vnew)[seg * CH + c], vf + 8 * c);
+    }
+    update(kf, vf, true);
   }
 
   // ---- merge: the 4 positions of each 16-lane row (DPP), then the rows ----
-  static_assert(sizeof(float) * G * kRows * D <= sizeof(sm.tile), "merge space fits in the tile buffers");
-  __syncthreads();  // every lane is done with the last tile: its LDS becomes merge space
   const int row = tid >> 4;
   const bool row_lead = (tid & 15) < 4;  // lane seg of position 0 of the row
 #pragma unroll
@@ -361,11 +308,11 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
   }
 }
 
-template <int D, int G>
+template <int D, int G, int NRING_OVERRIDE = 0>
 hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
-  // tiles in flight per block: as many as the VGPR budget allows next to
-  // the per-head softmax state (a tile is D / 2 VGPRs of K and V per lane)
-  constexpr int NRING = (G == 1) ? 3 : (G == 2 ? 2 : 1);
+  // tiles in flight per lane: a tile is D / 8 registers of K and V; the
+  // query quarter and the softmax state take (D / 4 + 2) G more
+  constexpr int NRING = NRING_OVERRIDE > 0 ? NRING_OVERRIDE : 1;
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
   return ext_launch(attn_split_kernel<D, G, NRING>, grid, dim3(kThreads), 0, s, ev, a);
 }
