@@ -173,6 +173,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--no-unfused", action="store_true",
+                    help="skip timing the op-by-op baseline (Alg. 1 + Alg. 2 operators, Concat reloading the cache)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="finish with a plain 256 MiB device copy (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -298,6 +300,43 @@ def main() -> int:
             log(f"graph capture failed: {ex!r}")
             graph_ms = None
 
+    # the op-by-op baseline on the same workload, replayed as a HIP graph
+    unfused = None
+    if not args.no_unfused:
+        lay.enable_unfused()
+        yu = [torch.empty_like(x0) for _ in range(nl)]
+
+        def step_unfused(s_):
+            x = x0
+            for li in range(nl):
+                lay.step_unfused(weights[li], x, pos, kcs[li], vcs[li], yu[li], s_)
+                x = yu[li]
+
+        step_unfused(stream)
+        torch.cuda.synchronize()
+        gu = torch.cuda.CUDAGraph()
+        su = torch.cuda.Stream()
+        su.wait_stream(stream)
+        with torch.cuda.stream(su):
+            with torch.cuda.graph(gu, stream=su):
+                step_unfused(su)
+        stream.wait_stream(su)
+        torch.cuda.synchronize()
+        for _ in range(2):
+            gu.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            gu.replay()
+        e1.record(stream)
+        e1.synchronize()
+        unf_ms = e0.elapsed_time(e1) / args.steps
+        same = bool(np.array_equal(L.from_device(yu[-1]), L.from_device(ys[-1])))
+        unfused = {"us_per_layer": round(unf_ms * 1e3 / nl, 3), "ms_per_step": round(unf_ms, 4),
+                   "launches_per_layer": 24, "y_bitwise_equal_to_fused": same}
+        log(f"unfused baseline (graph): {unf_ms:.3f} ms/step, {unf_ms * 1e3 / nl:.2f} us/layer")
+        del gu
+
     ms_step = min(stream_ms, graph_ms) if graph_ms is not None else stream_ms
     us_layer = ms_step * 1e3 / nl
     step_bytes = cfg.step_bytes(pos)
@@ -344,6 +383,8 @@ def main() -> int:
         "us_per_layer_graph": round(graph_ms * 1e3 / nl, 3) if graph_ms is not None else None,
         "kernels_us": {k: round(v, 3) for k, v in kern_us.items()},
         "roofline": roofline,
+        "unfused_baseline": (dict(unfused, speedup_of_fused=round(unfused["us_per_layer"] / us_layer, 3))
+                             if unfused else None),
         "cpu_baseline": cpu,
     }
     if args.calibrate_copy:

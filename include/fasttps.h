@@ -123,6 +123,25 @@ FASTTPS_API int fasttps_decode_step(fasttps_layer* layer, const fasttps_weights*
                         const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
                         void* y, void* stream);
 
+/* The op-by-op baseline: the same step computed the way the paper's
+ * standard implementation does it (Alg. 1: RoPE, Transpose, Concat, QK^T,
+ * Softmax, PV; Alg. 2: gate, SiLU, up, elementwise mul, down; RMSNorm, the
+ * separate Q, K, V, O projections and the residual adds as operators of
+ * their own), each operator a kernel whose inputs and outputs go through
+ * HBM, and the Concat rebuilding each sequence's K and V cache in a new
+ * buffer (the cache reload that GKVC removes, Section 3.1.1). It exists to
+ * measure the fused step against. Same arguments, results (within the same
+ * tolerances) and cache contract as fasttps_decode_step: slot pos[b] of the
+ * caller's caches is written, nothing else of them. Needs the baseline's
+ * scratch, allocated once per layer handle by fasttps_unfused_enable
+ * (blocking; about 2 B H_kv N_max d bf16 plus the fp32 intermediates, for
+ * max_batch sequences; freed with the layer). Returns FASTTPS_ERR_INVALID_ARG
+ * if the scratch was not enabled. */
+FASTTPS_API int fasttps_unfused_enable(fasttps_layer* layer);
+FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_weights* w, const void* x,
+                                const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
+                                void* y, void* stream);
+
 /* Test hook: copy one of the step's fp32 intermediates from the handle's
  * scratch into `dst` (device), on `stream`, after a fasttps_decode_step on the
  * same stream. `which` selects:

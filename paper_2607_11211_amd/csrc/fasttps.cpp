@@ -73,6 +73,9 @@ struct fasttps_layer {
   float* attn_o;
   float* h1;
   float* mlp_a;
+  // the op-by-op baseline's scratch (fasttps_unfused_enable)
+  void* uf_arena = nullptr;
+  UnfusedArgs uf{};
   // per-kernel timing (measurement hook)
   std::vector<hipEvent_t> prof_events;  // [cap][kernel][start, stop]
   int prof_cap = 0;
@@ -262,6 +265,10 @@ int fasttps_layer_destroy(fasttps_layer* l) {
   release_events(l);
   l->magic = kDeadMagic;
   hipError_t e = hipFree(l->arena);
+  if (l->uf_arena) {
+    const hipError_t e2 = hipFree(l->uf_arena);
+    if (e == hipSuccess) e = e2;
+  }
   delete l;
   if (e != hipSuccess) return hip_fail(e, "hipFree");
   return FASTTPS_OK;
@@ -383,9 +390,12 @@ int fasttps_weights_free(fasttps_weights* w) {
   return FASTTPS_OK;
 }
 
-int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
-                        int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
-  g_last_error.clear();
+namespace {
+
+// The checks shared by both step entry points; on success *maxp is the largest
+// position of the batch. Makes no HIP call.
+int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
+               void* k_cache, void* v_cache, void* y, int* maxp) {
   if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
   if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad weights handle");
   const fasttps_config& c = l->cfg;
@@ -396,11 +406,11 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
     return fail(FASTTPS_ERR_INVALID_ARG, "batch %d outside [1, %d]", batch, c.max_batch);
   if (!aligned16(x) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(y))
     return fail(FASTTPS_ERR_ALIGNMENT, "tensor pointers must be 16-byte aligned");
-  int maxp = 0;
+  int mp = 0;
   for (int b = 0; b < batch; ++b) {
     if (pos[b] < 0 || pos[b] >= c.max_seq)
       return fail(FASTTPS_ERR_CACHE_FULL, "pos[%d] = %d outside [0, %d)", b, pos[b], c.max_seq);
-    maxp = std::max(maxp, pos[b]);
+    mp = std::max(mp, pos[b]);
   }
   const size_t D = c.hidden, d = c.head_dim;
   const size_t act_bytes = (size_t)batch * D * 2;
@@ -410,6 +420,20 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
     return fail(FASTTPS_ERR_INVALID_ARG, "y overlaps x or a cache");
   if (overlaps(k_cache, cache_bytes, v_cache, cache_bytes))
     return fail(FASTTPS_ERR_INVALID_ARG, "k_cache and v_cache overlap");
+  *maxp = mp;
+  return FASTTPS_OK;
+}
+
+}  // namespace
+
+int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
+                        int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
+  g_last_error.clear();
+  int maxp = 0;
+  const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
+  if (st) return st;
+  const fasttps_config& c = l->cfg;
+  const size_t D = c.hidden, d = c.head_dim;
 
   // attention split: about kTargetAttnBlocks blocks, 64-position tiles
   const int maxn = maxp + 1;
@@ -526,3 +550,87 @@ int fasttps_debug_read(fasttps_layer* l, int32_t which, int32_t batch, void* dst
 }
 
 }  // extern "C"
+
+int fasttps_unfused_enable(fasttps_layer* l) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (l->uf_arena) return FASTTPS_OK;
+  const fasttps_config& c = l->cfg;
+  const size_t B = c.max_batch, D = c.hidden, H = c.n_heads, Hkv = c.n_kv_heads, d = c.head_dim;
+  const size_t K = c.intermediate, N = c.max_seq;
+  const int pv_cap = unfused_pv_splits(c.max_seq);
+  // fp32 buffers, then the two bf16 concat buffers
+  const size_t f32[] = {B * D,       B * H * d, B * Hkv * d, B * Hkv * d, B * H * d, B * Hkv * d, B * H * d,
+                        B * Hkv * d, B * Hkv * d, B * H * N,  B * H * N,   B * H * (size_t)pv_cap * d,
+                        B * H * d,   B * D,     B * D,       B * D,       B * K,     B * K,       B * K,
+                        B * K,       B * D};
+  constexpr int kF = sizeof(f32) / sizeof(f32[0]);
+  size_t offs[kF + 2], total = 0;
+  for (int i = 0; i < kF; ++i) {
+    offs[i] = total;
+    total += align256(f32[i] * sizeof(float));
+  }
+  const size_t cat_bytes = B * Hkv * N * d * sizeof(uint16_t);
+  offs[kF] = total;
+  total += align256(cat_bytes);
+  offs[kF + 1] = total;
+  total += align256(cat_bytes);
+  void* arena = nullptr;
+  hipError_t e = hipMalloc(&arena, total);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(FASTTPS_ERR_OOM, "hipMalloc(%zu): %s", total, hipGetErrorString(e));
+  }
+  char* base = static_cast<char*>(arena);
+  float* p[kF];
+  for (int i = 0; i < kF; ++i) p[i] = reinterpret_cast<float*>(base + offs[i]);
+  UnfusedArgs& u = l->uf;
+  u.h = p[0]; u.q = p[1]; u.k = p[2]; u.v = p[3]; u.q_rope = p[4]; u.k_rope = p[5]; u.q_t = p[6];
+  u.k_t = p[7]; u.v_t = p[8]; u.S = p[9]; u.P = p[10]; u.pv_part = p[11]; u.O = p[12]; u.attn_out = p[13];
+  u.h1 = p[14]; u.h2 = p[15]; u.g = p[16]; u.sg = p[17]; u.up = p[18]; u.hp = p[19]; u.mlp_out = p[20];
+  u.kcat = reinterpret_cast<uint16_t*>(base + offs[kF]);
+  u.vcat = reinterpret_cast<uint16_t*>(base + offs[kF + 1]);
+  u.pv_cap = pv_cap;
+  l->uf_arena = arena;
+  return FASTTPS_OK;
+}
+
+int fasttps_decode_step_unfused(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
+                                int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
+  g_last_error.clear();
+  int maxp = 0;
+  const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
+  if (st) return st;
+  if (!l->uf_arena) return fail(FASTTPS_ERR_INVALID_ARG, "call fasttps_unfused_enable on this layer first");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != l->device) return fail(FASTTPS_ERR_INVALID_ARG, "current device %d is not the layer's device %d", dev, l->device);
+  const fasttps_config& c = l->cfg;
+  UnfusedArgs u = l->uf;
+  u.x = static_cast<const uint16_t*>(x);
+  u.attn_norm = w->attn_norm;
+  u.mlp_norm = w->mlp_norm;
+  u.w_qkv = w->w_qkv;
+  u.w_o = w->w_o;
+  u.w_gu = w->w_gu;
+  u.w_down = w->w_down;
+  u.k_cache = static_cast<uint16_t*>(k_cache);
+  u.v_cache = static_cast<uint16_t*>(v_cache);
+  u.y = static_cast<uint16_t*>(y);
+  u.rope_cos = l->rope_cos;
+  u.rope_sin = l->rope_sin;
+  u.batch = batch;
+  u.hidden = c.hidden;
+  u.n_heads = c.n_heads;
+  u.n_kv_heads = c.n_kv_heads;
+  u.head_dim = c.head_dim;
+  u.inter = c.intermediate;
+  u.max_seq = c.max_seq;
+  u.maxn = maxp + 1;
+  u.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
+  u.eps = c.rms_eps;
+  for (int b = 0; b < batch; ++b) u.pos.p[b] = pos[b];
+  if ((e = launch_unfused(u, static_cast<hipStream_t>(stream))) != hipSuccess) return hip_fail(e, "unfused launch");
+  return FASTTPS_OK;
+}

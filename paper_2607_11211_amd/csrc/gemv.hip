@@ -44,7 +44,9 @@ namespace {
 // kResidual:     out = x + W act                             (x bf16, act fp32; fp32 out)
 // kDownResidual: y = bf16(res + W act)                       (res, act fp32; bf16 out)
 // kGateUp:       a = SiLU(W_g h) * (W_u h), h = RMSNorm(h1)  (h1 fp32; fp32 out)
-enum class Mode { kNormQkv, kResidual, kDownResidual, kGateUp };
+// kPlain:        out = W act                                 (act fp32; fp32 out; the
+//                op-by-op baseline's projections)
+enum class Mode { kNormQkv, kResidual, kDownResidual, kGateUp, kPlain };
 
 constexpr int kNumCu = 256;
 constexpr int kWaves = 16;
@@ -108,7 +110,7 @@ __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
   const int b0 = blockIdx.y * BT;
   const int nb = min(BT, a.batch - b0);
   const int nch = a.din >> 3;                  // chunks of a half row (= of the activation)
-  const size_t row_chunks = (size_t)NH * nch;  // chunks of a stored row
+  const size_t row_chunks = (a.ld ? (size_t)a.ld : (size_t)NH * a.din) / 8;  // chunks of a stored row
   const int cbase = sh * kSeg;
   const int hoff = half * nch;
   const int nres = (a.rows + G - 1) / G;
@@ -360,6 +362,9 @@ hipError_t launch_down_residual(const GemvArgs& a, hipStream_t s, KernelEvents e
 }
 hipError_t launch_gate_up(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
   return launch_mode<Mode::kGateUp>(a, s, ev);
+}
+hipError_t launch_gemv_plain(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
+  return launch_mode<Mode::kPlain>(a, s, ev);
 }
 
 }  // namespace fasttps

@@ -41,6 +41,7 @@ struct GemvArgs {
   const float* res_f32;    // down: residual h1 [batch, rows] fp32
   uint16_t* out_bf16;      // down: y [batch, rows] bf16
   float eps;
+  int ld;                  // elements per stored row of w (0: din, or 2 din for gate/up)
 };
 
 // RMSNorm1(x) followed by the fused QKV projection (fp32 out, before RoPE).
@@ -52,6 +53,8 @@ hipError_t launch_down_residual(const GemvArgs& a, hipStream_t s, KernelEvents e
 // a = SiLU(W_gate h2) * (W_up h2), h2 = RMSNorm2(h1), over the interlaced
 // W_gu with tiles of one row (rows = K).
 hipError_t launch_gate_up(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
+// out = W act (fp32 in and out), rows of `ld` elements (the op-by-op baseline).
+hipError_t launch_gemv_plain(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
 struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
@@ -70,6 +73,26 @@ struct AttnArgs {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
 // combine the split partials into o
 hipError_t launch_attention_combine(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
+
+// The op-by-op baseline (Alg. 1 + Alg. 2, every intermediate through HBM).
+struct UnfusedArgs {
+  const uint16_t* x;                       // [B, D] bf16
+  const uint16_t *attn_norm, *mlp_norm;    // [D]
+  const uint16_t *w_qkv, *w_o, *w_gu, *w_down;  // packed weights
+  uint16_t *k_cache, *v_cache;             // [B, H_kv, N_max, d], slot pos_b written
+  uint16_t* y;                             // [B, D] bf16
+  const double *rope_cos, *rope_sin;       // [N_max, d/2]
+  float *h, *q, *k, *v, *q_rope, *k_rope, *q_t, *k_t, *v_t;  // fp32 intermediates
+  uint16_t *kcat, *vcat;                   // the concatenated caches [B, H_kv, N_max, d]
+  float *S, *P;                            // [B, H, N_max]
+  float* pv_part;                          // [B, H, pv_cap, d]
+  float *O, *attn_out, *h1, *h2, *g, *sg, *up, *hp, *mlp_out;
+  int batch, hidden, n_heads, n_kv_heads, head_dim, inter, max_seq, maxn, pv_cap;
+  float scale, eps;
+  PosArray pos;
+};
+hipError_t launch_unfused(const UnfusedArgs& u, hipStream_t s);
+int unfused_pv_splits(int max_seq);
 
 // packing (cold path)
 hipError_t launch_interlace_gate_up(const uint16_t* gate, const uint16_t* up, uint16_t* dst, int inter,

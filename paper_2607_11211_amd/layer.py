@@ -29,6 +29,7 @@ DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
 
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
+           "fasttps_unfused_enable", "fasttps_decode_step_unfused",
            "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 6
 
@@ -60,6 +61,8 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_layer_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]
     lib.fasttps_weights_pack.argtypes = [vp, ctypes.POINTER(WeightsDesc), vp, ctypes.POINTER(vp)]
     lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
+    lib.fasttps_decode_step_unfused.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
+    lib.fasttps_unfused_enable.argtypes = [vp]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
     lib.fasttps_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
@@ -73,7 +76,7 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_last_error.restype = ctypes.c_char_p
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
-                 "fasttps_layer_destroy"):
+                 "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -155,6 +158,19 @@ class Layer:
                                        p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
                                        _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step")
+
+    def enable_unfused(self) -> None:
+        """Allocate the op-by-op baseline's scratch (once per handle)."""
+        _check(LIB.fasttps_unfused_enable(self.handle), "fasttps_unfused_enable")
+
+    def step_unfused(self, weights: Weights, x, pos, k_cache, v_cache, y, stream=None) -> None:
+        """Enqueue one step of the op-by-op baseline (same contract as step)."""
+        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
+        batch = int(p.shape[0])
+        _check(LIB.fasttps_decode_step_unfused(self.handle, weights.handle, _ptr(x),
+                                               p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
+                                               _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
+               "fasttps_decode_step_unfused")
 
     def debug_read(self, which: int, batch: int, dst, stream=None) -> None:
         _check(LIB.fasttps_debug_read(self.handle, int(which), int(batch), _ptr(dst),

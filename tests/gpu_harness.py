@@ -34,8 +34,9 @@ def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
     return np.abs(key(a_bits) - key(b_bits))
 
 
-def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False):
-    """One decode step on cuda:0 through the C ABI. Returns host copies."""
+def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=False):
+    """One decode step on cuda:0 through the C ABI (the op-by-op baseline when
+    unfused). Returns host copies."""
     import torch
     from paper_2607_11211_amd import layer as L
     lay = layer if layer is not None else L.Layer(cfg)
@@ -49,7 +50,12 @@ def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False):
     vc = L.to_device(inp.v_cache)
     y = torch.empty_like(x)
     B = cfg.batch
-    lay.step(W, x, inp.pos, kc, vc, y)
+    if unfused:
+        lay.enable_unfused()
+        lay.step_unfused(W, x, inp.pos, kc, vc, y)
+        debug = False
+    else:
+        lay.step(W, x, inp.pos, kc, vc, y)
     out = {}
     if debug:
         dev = x.device

@@ -38,6 +38,12 @@ def test_library_exports_every_declared_symbol(L):
     assert set(declared_functions()) == set(L.EXPORTS)
 
 
+def test_unfused_entry_points_reject_bad_handles(L):
+    assert L.LIB.fasttps_unfused_enable(None) == L.ERR_BAD_HANDLE
+    p = (ctypes.c_int32 * 1)(0)
+    assert L.LIB.fasttps_decode_step_unfused(None, None, None, p, 1, None, None, None, None) == L.ERR_BAD_HANDLE
+
+
 def test_probe_library_exports_its_header():
     """The measurement aid (stream-read probe) is a library of its own with
     its own header; it rejects bad arguments before touching the GPU."""
