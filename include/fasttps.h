@@ -142,6 +142,14 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
                                 const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
                                 void* y, void* stream);
 
+/* Accuracy-study hook: when enabled, later steps of this layer handle round
+ * the softmax weights to bf16 before the PV accumulation, as FlashAttention
+ * does with its bf16 P (the softmax row sum stays fp32), so the attention
+ * output error of the two can be compared over the context length (the
+ * paper's Fig. 8 comparison, Section 5.4). Off by default; a step with it on
+ * is not the FastTPS step. */
+FASTTPS_API int fasttps_set_attention_p_bf16(fasttps_layer* layer, int32_t enable);
+
 /* Test hook: copy one of the step's fp32 intermediates from the handle's
  * scratch into `dst` (device), on `stream`, after a fasttps_decode_step on the
  * same stream. `which` selects:

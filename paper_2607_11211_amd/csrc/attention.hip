@@ -73,7 +73,10 @@ __device__ __forceinline__ void tile_load(v4u (&k)[D / 32], v4u (&v)[D / 32], co
   }
 }
 
-template <int D, int G, int NRING>
+// PBF16: the softmax weights enter PV rounded to bf16, as FlashAttention's
+// bf16 P does (the row sum l keeps the fp32 weights); the accuracy study
+// compares this with the fp32 path. The step itself uses PBF16 = false.
+template <int D, int G, int NRING, bool PBF16>
 __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   constexpr int SEG = D / 4;   // elements of a position row per lane
   constexpr int CH = D / 32;   // 16-byte chunks per lane (K and V each)
@@ -169,8 +172,9 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
         const float cf = merge_factor(m[h], mn);
         const float p = __expf(sc - mn);
         l[h] = fmaf(l[h], cf, p);
+        const float pv = PBF16 ? bf16_to_f32(f32_to_bf16(p)) : p;
 #pragma unroll
-        for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, p * vf[e]);
+        for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, pv * vf[e]);
         m[h] = mn;
       }
     }
@@ -314,7 +318,8 @@ hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   // query quarter and the softmax state take (D / 4 + 2) G more
   constexpr int NRING = NRING_OVERRIDE > 0 ? NRING_OVERRIDE : 1;
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
-  return ext_launch(attn_split_kernel<D, G, NRING>, grid, dim3(kThreads), 0, s, ev, a);
+  if (a.p_bf16) return ext_launch(attn_split_kernel<D, G, NRING, true>, grid, dim3(kThreads), 0, s, ev, a);
+  return ext_launch(attn_split_kernel<D, G, NRING, false>, grid, dim3(kThreads), 0, s, ev, a);
 }
 
 template <int D>

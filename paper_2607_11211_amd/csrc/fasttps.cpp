@@ -65,6 +65,7 @@ struct fasttps_layer {
   fasttps_config cfg;
   int device;
   int nsplit_cap;
+  int p_bf16 = 0;  // accuracy study switch (fasttps_set_attention_p_bf16)
   void* arena;
   double* rope_cos;
   double* rope_sin;
@@ -487,6 +488,7 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   aa.nsplit = nsplit;
   aa.nsplit_cap = l->nsplit_cap;
   aa.scale = (float)(1.0 / std::sqrt((double)d));
+  aa.p_bf16 = l->p_bf16;
   for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
   if ((e = launch_attention(aa, s, ev[1])) != hipSuccess) return hip_fail(e, "attention launch");
   if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
@@ -632,5 +634,12 @@ int fasttps_decode_step_unfused(fasttps_layer* l, const fasttps_weights* w, cons
   u.eps = c.rms_eps;
   for (int b = 0; b < batch; ++b) u.pos.p[b] = pos[b];
   if ((e = launch_unfused(u, static_cast<hipStream_t>(stream))) != hipSuccess) return hip_fail(e, "unfused launch");
+  return FASTTPS_OK;
+}
+
+int fasttps_set_attention_p_bf16(fasttps_layer* l, int32_t enable) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  l->p_bf16 = enable ? 1 : 0;
   return FASTTPS_OK;
 }

@@ -67,6 +67,7 @@ struct AttnArgs {
   int batch, n_heads, n_kv_heads, head_dim, max_seq;
   int split_len, nsplit, nsplit_cap;
   float scale;             // 1/sqrt(d)
+  int p_bf16;              // accuracy study: softmax weights rounded to bf16 before PV
   PosArray pos;
 };
 // per split: RoPE, append, partial softmax state (m, l, o)

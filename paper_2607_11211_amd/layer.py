@@ -29,7 +29,7 @@ DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
 
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
-           "fasttps_unfused_enable", "fasttps_decode_step_unfused",
+           "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
            "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 6
 
@@ -63,6 +63,7 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     lib.fasttps_decode_step_unfused.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     lib.fasttps_unfused_enable.argtypes = [vp]
+    lib.fasttps_set_attention_p_bf16.argtypes = [vp, i32]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
     lib.fasttps_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
@@ -76,7 +77,8 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_last_error.restype = ctypes.c_char_p
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
-                 "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused"):
+                 "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
+                 "fasttps_set_attention_p_bf16"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -171,6 +173,10 @@ class Layer:
                                                p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
                                                _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step_unfused")
+
+    def set_attention_p_bf16(self, enable: bool) -> None:
+        """Accuracy study only: round the softmax weights to bf16 before PV."""
+        _check(LIB.fasttps_set_attention_p_bf16(self.handle, 1 if enable else 0), "fasttps_set_attention_p_bf16")
 
     def debug_read(self, which: int, batch: int, dst, stream=None) -> None:
         _check(LIB.fasttps_debug_read(self.handle, int(which), int(batch), _ptr(dst),

@@ -1,0 +1,65 @@
+"""Attention-output accuracy against fp64 over the context length (the
+paper's Fig. 8 study, Section 5.4), on MI355X through the C ABI.
+
+For N_t = pos + 1 from 128 to 32768 cached entries at the Phi-3 attention
+shape (32 heads of 96), the step's attention output o (fp32) is compared with
+the oracle's fp64 o: error = max over heads of max |o - o_ref| / max |o_ref|.
+The same inputs run again with the softmax weights rounded to bf16 before PV
+(FlashAttention's bf16 P). The fp32 path must stay within the parity bar at
+every length and well below the paper's 0.22 %; the bf16-P variant is
+reported next to it and must be the less accurate of the two.
+"""
+import numpy as np
+import pytest
+
+from gpu_harness import O_TOL, log, run_gpu
+from oracle import ref
+from paper_2607_11211_amd import inputs
+from paper_2607_11211_amd.configs import LayerConfig
+
+pytestmark = pytest.mark.gpu
+
+LENGTHS = (128, 512, 2048, 8192, 32768)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_11211_amd.layer  # noqa: F401  (fails loudly if the library is missing)
+
+
+def _cfg(i, n):
+    # Phi-3 attention (D 3072, 32 x 96); a narrow MLP keeps the oracle quick and
+    # does not touch o
+    return LayerConfig(name=f"acc_n{n}", index=30 + i, batch=1, hidden=3072, n_heads=32, n_kv_heads=32,
+                       head_dim=96, intermediate=1024, rope_base=10000.0, max_seq=n + 64, pos=(n - 1,))
+
+
+def _err(o_gpu, o_ref, cfg):
+    o = o_gpu.reshape(cfg.batch, cfg.n_heads, cfg.head_dim)
+    return float(np.max(np.abs(o - o_ref) / np.max(np.abs(o_ref), axis=2, keepdims=True)))
+
+
+def test_attention_error_over_context_length():
+    from paper_2607_11211_amd import layer as L
+    rows = []
+    for i, n in enumerate(LENGTHS):
+        cfg = _cfg(i, n)
+        inp = inputs.make_layer_inputs(cfg)
+        r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, ref.widen_weights(inp.weights))
+        lay = L.Layer(cfg)
+        try:
+            e32 = _err(run_gpu(cfg, inp, layer=lay)["o"], r["o"], cfg)
+            lay.set_attention_p_bf16(True)
+            ebf = _err(run_gpu(cfg, inp, layer=lay)["o"], r["o"], cfg)
+        finally:
+            lay.destroy()
+        rows.append((n, e32, ebf))
+        log(f"N_t {n:6d}: max rel err fp32 path {e32:.3e}, bf16 P {ebf:.3e}")
+    log("accuracy table (N_t, fp32 path, bf16 P): " + "; ".join(f"{n} {a:.2e} {b:.2e}" for n, a, b in rows))
+    for n, e32, ebf in rows:
+        assert e32 <= O_TOL, f"N_t {n}: attention output error {e32:.3e} above {O_TOL}"
+        assert e32 < 2.2e-3
+        assert ebf > e32, f"N_t {n}: bf16 P not less accurate ({ebf:.3e} vs {e32:.3e})"
