@@ -164,6 +164,89 @@ def read_ceiling(nbytes: int = 4 << 30):
     return best
 
 
+def sweep(args) -> int:
+    """Latency sweeps (the paper's Fig. 6 axes): the fused layer and the op-by-op
+    baseline per layer step, over the context length at the Phi-3 shape and
+    over the head dimension at the Table 1 shapes (L3.2 d 64, P3 d 96, L2 d 128)
+    at 2048 entries. Four rotating layer copies keep the data out of the
+    Infinity Cache between visits. One JSON line per point."""
+    import torch
+    from paper_2607_11211_amd import configs
+    from paper_2607_11211_amd import layer as L
+    from paper_2607_11211_amd.configs import LayerConfig
+    torch.cuda.set_device(0)
+    phi3 = dict(hidden=3072, n_heads=32, n_kv_heads=32, head_dim=96, intermediate=8192, rope_base=10000.0)
+    points = [("phi3", n, phi3) for n in (512, 1024, 2048, 4096, 8192, 16384, 32768)]
+    points += [("llama3.2-1b-like (d 64)", 2048, dict(hidden=2048, n_heads=32, n_kv_heads=32, head_dim=64,
+                                                        intermediate=8192, rope_base=10000.0)),
+               ("phi3 (d 96)", 2048, phi3),
+               ("llama2-7b (d 128)", 2048, dict(hidden=4096, n_heads=32, n_kv_heads=32, head_dim=128,
+                                                 intermediate=11008, rope_base=10000.0)),
+               ("llama3-8b (GQA 32/8, d 128)", 2048, dict(hidden=4096, n_heads=32, n_kv_heads=8, head_dim=128,
+                                                           intermediate=14336, rope_base=500000.0))]
+    ncopy = 4
+    for name, n, shape in points:
+        cfg = LayerConfig(name=f"sweep_{n}", index=40, batch=1, max_seq=n + 64, pos=(n,), **shape)
+        pos = np.array([n], dtype=np.int32)
+        lay = L.Layer(cfg)
+        lay.enable_unfused()
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(0xFA57 + n)
+        ws, kcs, vcs = [], [], []
+        for li in range(ncopy):
+            w, kc, vc = device_layer(cfg, li, pos, gen)
+            ws.append(lay.pack(w))
+            del w
+            kcs.append(kc)
+            vcs.append(vc)
+        x0 = torch.randn((1, cfg.hidden), generator=gen, device="cuda").to(torch.bfloat16).view(torch.int16)
+        ys = [torch.empty_like(x0) for _ in range(ncopy)]
+        stream = torch.cuda.current_stream()
+
+        def timed(fn):
+            fn(stream)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(stream)
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    fn(s)
+            stream.wait_stream(s)
+            torch.cuda.synchronize()
+            for _ in range(3):
+                g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(args.steps):
+                g.replay()
+            e1.record(stream)
+            e1.synchronize()
+            return e0.elapsed_time(e1) / args.steps * 1e3 / ncopy
+
+        def fused(s):
+            for li in range(ncopy):
+                lay.step(ws[li], x0, pos, kcs[li], vcs[li], ys[li], s)
+
+        def unfused(s):
+            for li in range(ncopy):
+                lay.step_unfused(ws[li], x0, pos, kcs[li], vcs[li], ys[li], s)
+
+        us_f, us_u = timed(fused), timed(unfused)
+        step_bytes = cfg.step_bytes(pos)
+        print(json.dumps({"sweep": name, "kv_entries": n, "d": cfg.head_dim, "us_fused": round(us_f, 2),
+                          "us_unfused": round(us_u, 2), "speedup": round(us_u / us_f, 3),
+                          "fused_hbm_gbps": round(step_bytes / (us_f * 1e-6) / 1e9, 1),
+                          "bytes_per_step": step_bytes}), flush=True)
+        for w in ws:
+            w.free()
+        lay.destroy()
+        del kcs, vcs, ys
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -173,6 +256,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--sweep", action="store_true",
+                    help="latency sweeps over the context length and the head dimension (fused vs op-by-op), "
+                         "one JSON line per point, instead of the benchmark")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip timing the op-by-op baseline (Alg. 1 + Alg. 2 operators, Concat reloading the cache)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -190,6 +276,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py: no GPU", file=sys.stderr)
         return 1
+    if args.sweep:
+        return sweep(args)
     torch.cuda.set_device(0)
     cfg = configs.get(args.workload)
     nl = cfg.layers
