@@ -16,21 +16,35 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// h[b] = x[b] / sqrt(mean(x[b]^2) + eps) * gamma; x bf16 or fp32 (one block per row)
+// h[b] = x[b] / sqrt(mean(x[b]^2) + eps) * gamma; x bf16 or fp32 (one block of
+// 1024 threads per row; the row is read once into registers)
+constexpr int kNormThreads = 1024;
+constexpr int kNormPer = 8;  // hidden <= 8192, the layer's limit
+
 template <bool BF16_IN>
-__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const void* __restrict__ x, const uint16_t* __restrict__ gamma,
-                                                           float* __restrict__ h, int D, float eps) {
-  __shared__ float red[kThreads / kWave];
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const void* __restrict__ x,
+                                                               const uint16_t* __restrict__ gamma,
+                                                               float* __restrict__ h, int D, float eps) {
+  __shared__ float red[kNormThreads / kWave];
   const int b = blockIdx.x;
-  auto xv = [&](int i) -> float {
-    return BF16_IN ? bf16_to_f32(static_cast<const uint16_t*>(x)[(size_t)b * D + i])
-                   : static_cast<const float*>(x)[(size_t)b * D + i];
-  };
+  float xv[kNormPer];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < D; i += kThreads) ss = fmaf(xv(i), xv(i), ss);
+#pragma unroll
+  for (int k = 0; k < kNormPer; ++k) {
+    const int i = threadIdx.x + k * kNormThreads;
+    const int ic = min(i, D - 1);
+    const float v = BF16_IN ? bf16_to_f32(static_cast<const uint16_t*>(x)[(size_t)b * D + ic])
+                            : static_cast<const float*>(x)[(size_t)b * D + ic];
+    xv[k] = i < D ? v : 0.f;
+    ss = fmaf(xv[k], xv[k], ss);
+  }
   const float tot = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(tot / (float)D + eps);
-  for (int i = threadIdx.x; i < D; i += kThreads) h[(size_t)b * D + i] = xv(i) * inv * bf16_to_f32(gamma[i]);
+#pragma unroll
+  for (int k = 0; k < kNormPer; ++k) {
+    const int i = threadIdx.x + k * kNormThreads;
+    if (i < D) h[(size_t)b * D + i] = xv[k] * inv * bf16_to_f32(gamma[i]);
+  }
 }
 
 // RoPE of `nh` heads of d values per sequence (rotate-half, fp64 cos/sin row of
@@ -252,7 +266,7 @@ hipError_t launch_unfused(const UnfusedArgs& u, hipStream_t s) {
     return launch_gemv_plain(g, s);
   };
   // ---- attention block (Alg. 1) ------------------------------------------
-  hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(kThreads), 0, s, u.x, u.attn_norm, u.h, D, u.eps);
+  hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(kNormThreads), 0, s, u.x, u.attn_norm, u.h, D, u.eps);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = gemv(u.w_qkv, qd, D, 0, u.h, u.q)) != hipSuccess) return e;
   if ((e = gemv(u.w_qkv + (size_t)qd * D, kvd, D, 0, u.h, u.k)) != hipSuccess) return e;
@@ -288,7 +302,7 @@ hipError_t launch_unfused(const UnfusedArgs& u, hipStream_t s) {
   hipLaunchKernelGGL((add_kernel<true, false>), grid1(B * D), dim3(kThreads), 0, s, u.x, u.attn_out, u.h1, B * D);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   // ---- MLP block (Alg. 2) ------------------------------------------------
-  hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(kThreads), 0, s, u.h1, u.mlp_norm, u.h2, D, u.eps);
+  hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(kNormThreads), 0, s, u.h1, u.mlp_norm, u.h2, D, u.eps);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   // Step 1: gate projection (the even rows of the interlaced W_gu), Step 2: SiLU
   if ((e = gemv(u.w_gu, K, D, 2 * D, u.h2, u.g)) != hipSuccess) return e;
