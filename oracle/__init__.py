@@ -13,6 +13,8 @@ Modules:
                    checked in fp64
   brute         -- the same layer again in pure Python scalars (math.fsum,
                    exact Fraction rounding), for tiny shapes
+  kvquant       -- 8-bit KV cache formats (FP8 E4M3, INT8 with per-head
+                   scales) for the layer with a quantized cache
 
 Parity status of each function is stated in its module header.
 """

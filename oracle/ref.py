@@ -14,7 +14,9 @@ in the design notes of the repository):
     same for every head, position = N_p (0-based index of the new token);
   * softmax scale 1/sqrt(d); the query attends exactly entries [0, N_p];
   * grouped-query attention: query head h reads KV head h // (H / H_kv);
-  * attention consumes the appended K/V as stored, i.e. after bf16 rounding.
+  * attention consumes the appended K/V as stored, i.e. after bf16 rounding
+    (after 8-bit quantization for an 8-bit cache, whose format is read in
+    ``kvquant``).
 
 Parity: pinned. Each function is checked by the CPU tests against brute force
 in pure Python scalars, closed forms and invariants (RoPE group and
@@ -205,12 +207,21 @@ def widen_weights(weights_bits: Mapping[str, np.ndarray]) -> Dict[str, np.ndarra
 
 
 def decode_layer(x_bits, pos, k_cache_bits, v_cache_bits, weights, *, n_heads: int,
-                 n_kv_heads: int, rope_base: float, rms_eps: float) -> Dict[str, np.ndarray]:
+                 n_kv_heads: int, rope_base: float, rms_eps: float, kv=None,
+                 new_entries=None) -> Dict[str, np.ndarray]:
     """One token-phase step of one decoder layer, per sequence b.
 
     Inputs: x_bits [B, D] bf16 bits; pos [B] (N_p per sequence); caches
     [B, H_kv, N_max, d] bf16 bits holding entries [0, N_p); weights as bf16 bits
     in nn.Linear layout, or already widened by ``widen_weights``.
+
+    With ``kv`` (a ``kvquant.KvQuant``: 8-bit format and per-KV-head scales)
+    the caches hold 8-bit codes instead: a cached entry of KV head g is read as
+    scale_g * value(code), and the entries appended in step 4 are the codes of
+    k_rope / k_scale_g and v / v_scale_g. ``new_entries`` = (k, v), arrays
+    [B, H_kv, d] of bits or codes, replaces the entries step 4 would append
+    (teacher forcing: where a rounding of the GPU's own entry lands on the
+    neighbouring value, the rest of the step is compared on that entry).
 
     Steps (Section 2.2 / Alg. 3 for attention, Eq. mlp_main for the MLP):
       1. h  = RMSNorm1(x)
@@ -224,6 +235,8 @@ def decode_layer(x_bits, pos, k_cache_bits, v_cache_bits, weights, *, n_heads: i
       9. y  = h1 + W_down a, and bf16(y)
     Returns every intermediate, float64 unless named *_bits.
     """
+    if kv is not None:
+        from . import kvquant
     W = weights if weights["w_q"].dtype == np.float64 else widen_weights(weights)
     X = bf16_bits_to_f64(x_bits)
     B, D = X.shape
@@ -235,7 +248,8 @@ def decode_layer(x_bits, pos, k_cache_bits, v_cache_bits, weights, *, n_heads: i
     out = {
         "h": np.zeros((B, D)), "q": np.zeros((B, H, d)), "k": np.zeros((B, G, d)),
         "v": np.zeros((B, G, d)), "q_rope": np.zeros((B, H, d)), "k_rope": np.zeros((B, G, d)),
-        "k_new_bits": np.zeros((B, G, d), np.uint16), "v_new_bits": np.zeros((B, G, d), np.uint16),
+        "k_new_bits": np.zeros((B, G, d), np.uint16 if kv is None else np.uint8),
+        "v_new_bits": np.zeros((B, G, d), np.uint16 if kv is None else np.uint8),
         "o": np.zeros((B, H, d)), "h1": np.zeros((B, D)), "h2": np.zeros((B, D)),
         "gate": np.zeros((B, K)), "up": np.zeros((B, K)), "a": np.zeros((B, K)),
         "y": np.zeros((B, D)),
@@ -250,14 +264,22 @@ def decode_layer(x_bits, pos, k_cache_bits, v_cache_bits, weights, *, n_heads: i
         v = linear(W["w_v"], h).reshape(G, d)
         q_r = rope(q, p, rope_base)
         k_r = rope(k, p, rope_base)
-        k_new = f64_to_bf16_bits(k_r)
-        v_new = f64_to_bf16_bits(v)
+        if kv is None:
+            k_new = f64_to_bf16_bits(k_r)
+            v_new = f64_to_bf16_bits(v)
+            k_val = v_val = lambda bits, g: bf16_bits_to_f64(bits)
+        else:
+            k_new = np.stack([kvquant.quantize(k_r[g], kv.k_scale[g], kv.fmt) for g in range(G)])
+            v_new = np.stack([kvquant.quantize(v[g], kv.v_scale[g], kv.fmt) for g in range(G)])
+            k_val = lambda codes, g: kvquant.dequantize(codes, kv.k_scale[g], kv.fmt)
+            v_val = lambda codes, g: kvquant.dequantize(codes, kv.v_scale[g], kv.fmt)
+        if new_entries is not None:
+            k_new = np.asarray(new_entries[0][b], dtype=k_new.dtype)
+            v_new = np.asarray(new_entries[1][b], dtype=v_new.dtype)
         o = np.zeros((H, d))
         for g in range(G):
-            kc = np.concatenate([bf16_bits_to_f64(k_cache_bits[b, g, :p]),
-                                 bf16_bits_to_f64(k_new[g])[None, :]], axis=0)
-            vc = np.concatenate([bf16_bits_to_f64(v_cache_bits[b, g, :p]),
-                                 bf16_bits_to_f64(v_new[g])[None, :]], axis=0)
+            kc = np.concatenate([k_val(k_cache_bits[b, g, :p], g), k_val(k_new[g], g)[None, :]], axis=0)
+            vc = np.concatenate([v_val(v_cache_bits[b, g, :p], g), v_val(v_new[g], g)[None, :]], axis=0)
             for hq in range(g * group, (g + 1) * group):
                 o[hq], _ = attention_one_query(q_r[hq], kc, vc)
         h1 = X[b] + linear(W["w_o"], o.reshape(H * d))
@@ -273,8 +295,8 @@ def decode_layer(x_bits, pos, k_cache_bits, v_cache_bits, weights, *, n_heads: i
     return out
 
 
-def decode_layer_cfg(cfg, x_bits, pos, k_cache_bits, v_cache_bits, weights):
+def decode_layer_cfg(cfg, x_bits, pos, k_cache_bits, v_cache_bits, weights, kv=None, new_entries=None):
     """decode_layer with the head counts, RoPE base and eps taken from a shape record."""
     return decode_layer(x_bits, pos, k_cache_bits, v_cache_bits, weights,
                         n_heads=cfg.n_heads, n_kv_heads=cfg.n_kv_heads,
-                        rope_base=cfg.rope_base, rms_eps=cfg.rms_eps)
+                        rope_base=cfg.rope_base, rms_eps=cfg.rms_eps, kv=kv, new_entries=new_entries)

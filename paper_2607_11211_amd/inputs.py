@@ -9,6 +9,13 @@ Recipe (the same bits feed the oracle and the library):
     sentinels (0x7FC0 in K, 0xFFC0 in V): a read of a reserved slot poisons
     the output, and a missing append leaves a NaN behind;
   * ragged workloads draw pos_b uniformly from [lo, hi];
+  * 8-bit caches (FP8 E4M3 or INT8 codes, one scale per KV head) are drawn as
+    codes, not converted from values: E4M3 entries take every finite code
+    (both signs, subnormals up to +-448) with equal probability, INT8 entries
+    take [-127, 127] uniformly; the per-head scales are (0.5 + U[0, 1)) / 64
+    for E4M3 and (0.5 + U[0, 1)) / 32 for INT8, as float32; reserved slots
+    hold the E4M3 NaN codes (0x7F in K, 0xFF in V) or -128, which no INT8
+    entry uses;
   * each tensor has its own stream: PCG64 seeded with
     SeedSequence([0xFA57, seed, workload index, layer, tensor id, chunk]).
     Large tensors are filled in fixed 4 Mi-element chunks, so the bits do not
@@ -34,6 +41,11 @@ V_SENTINEL = 0xFFC0
 CHUNK = 1 << 22
 
 T_X, T_ATTN_NORM, T_WQ, T_WK, T_WV, T_WO, T_MLP_NORM, T_WG, T_WU, T_WD, T_KC, T_VC, T_POS = range(13)
+T_KC8, T_VC8, T_KS, T_VS = range(13, 17)
+
+KV8_FORMATS = ("fp8_e4m3", "int8")
+K8_SENTINEL = {"fp8_e4m3": 0x7F, "int8": 0x80}
+V8_SENTINEL = {"fp8_e4m3": 0xFF, "int8": 0x80}
 
 WEIGHT_NAMES = ("attn_norm", "w_q", "w_k", "w_v", "w_o", "mlp_norm", "w_gate", "w_up", "w_down")
 
@@ -138,6 +150,46 @@ def make_cache(cfg: LayerConfig, pos: np.ndarray, which: str, layer: int = 0, se
         vals = _normal_bf16(_words(cfg, seed, layer, tid) + [b], G * p * d, 1.0)
         cache[b, :, :p, :] = vals.reshape(G, p, d)
     return cache
+
+
+def _codes8(seed_words, n: int, fmt: str) -> np.ndarray:
+    """n random 8-bit cache codes of the format, filled chunk by chunk."""
+    out = np.empty(n, dtype=np.uint8)
+    for c in range((n + CHUNK - 1) // CHUNK):
+        lo, hi = c * CHUNK, min(n, (c + 1) * CHUNK)
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(list(seed_words) + [c])))
+        if fmt == "fp8_e4m3":
+            r = rng.integers(0, 254, size=hi - lo)       # 254 finite codes: skip 0x7F and 0xFF
+            out[lo:hi] = np.where(r < 0x7F, r, r + 1).astype(np.uint8)
+        elif fmt == "int8":
+            out[lo:hi] = rng.integers(-127, 128, size=hi - lo).astype(np.int8).view(np.uint8)
+        else:
+            raise ValueError(f"unknown 8-bit format {fmt!r}")
+    return out
+
+
+def make_cache8(cfg: LayerConfig, pos: np.ndarray, which: str, fmt: str, layer: int = 0,
+                seed: int = 0) -> np.ndarray:
+    """8-bit KV cache [B, H_kv, N_max, d] of codes: random codes in [0, pos_b), the sentinel elsewhere."""
+    tid, sentinel = (T_KC8, K8_SENTINEL[fmt]) if which == "k" else (T_VC8, V8_SENTINEL[fmt])
+    B, G, N, d = cfg.batch, cfg.n_kv_heads, cfg.max_seq, cfg.head_dim
+    cache = np.full((B, G, N, d), sentinel, dtype=np.uint8)
+    for b in range(B):
+        p = int(pos[b])
+        if p <= 0:
+            continue
+        cache[b, :, :p, :] = _codes8(_words(cfg, seed, layer, tid) + [b], G * p * d, fmt).reshape(G, p, d)
+    return cache
+
+
+def make_kv_scales(cfg: LayerConfig, which: str, fmt: str, layer: int = 0, seed: int = 0) -> np.ndarray:
+    """Per-KV-head scales of an 8-bit cache, float32 [H_kv]."""
+    if fmt not in KV8_FORMATS:
+        raise ValueError(f"unknown 8-bit format {fmt!r}")
+    tid = T_KS if which == "k" else T_VS
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(_words(cfg, seed, layer, tid))))
+    div = np.float32(64.0 if fmt == "fp8_e4m3" else 32.0)
+    return ((np.float32(0.5) + rng.random(cfg.n_kv_heads, dtype=np.float32)) / div).astype(np.float32)
 
 
 @dataclass

@@ -35,7 +35,7 @@ MUTATIONS = {
     "silu_sign": ("return z / (1.0 + np.exp(-z))", "return z / (1.0 + np.exp(z))"),
     "gate_up_swapped": ("a = silu(g) * u", "a = silu(u) * g"),
     "wq_transposed": ('q = linear(W["w_q"], h).reshape(H, d)', 'q = linear(W["w_q"].T, h).reshape(H, d)'),
-    "unrounded_new_key": ("bf16_bits_to_f64(k_new[g])[None, :]], axis=0)", "k_r[g][None, :]], axis=0)"),
+    "unrounded_new_key": ("k_val(k_new[g], g)[None, :]", "k_r[g][None, :]"),
     "wrong_mlp_gain": ('h2 = rms_norm(h1, W["mlp_norm"], rms_eps)', 'h2 = rms_norm(h1, W["attn_norm"], rms_eps)'),
     "bf16_truncates": ("q = np.rint(np.ldexp(ax, -qexp))", "q = np.floor(np.ldexp(ax, -qexp))"),
     "bf16_ties_up": ("q = np.rint(np.ldexp(ax, -qexp))", "q = np.floor(np.ldexp(ax, -qexp) + 0.5)"),
