@@ -123,6 +123,36 @@ FASTTPS_API int fasttps_decode_step(fasttps_layer* layer, const fasttps_weights*
                         const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
                         void* y, void* stream);
 
+/* 8-bit KV cache formats for fasttps_decode_step_kv8. */
+#define FASTTPS_KV_FP8_E4M3 1 /* OCP E4M3: bias 7, subnormals, largest finite 448, 0x7F/0xFF NaN */
+#define FASTTPS_KV_INT8 2     /* two's complement, entries in [-127, 127] */
+
+/* One decode step over an 8-bit KV cache. The paper holds its cache layout
+ * and append compatible with a quantized cache (Section 6.2, and Section 2.4,
+ * which counts the quantized cache's concatenation among the memory
+ * reorganisation operators) without fixing a format; this is the reading
+ * implemented:
+ *   kv_format  FASTTPS_KV_FP8_E4M3 or FASTTPS_KV_INT8
+ *   k_cache, v_cache
+ *              device, [batch, H_kv, N_max, d] of 8-bit codes, the GKVC layout
+ *              of Eq. 1 with one byte per element (16-byte aligned). An entry
+ *              of KV head g means k_scale[g] * value(code) (v_scale[g] for V).
+ *   k_scale, v_scale
+ *              host, [H_kv] float: the per-KV-head scales, positive and
+ *              finite; they are copied into the launch, so a captured graph
+ *              keeps the values of the call that was captured.
+ * The new entry of each (b, g) is rounded once, in double precision, to the
+ * nearest code of k_rope / k_scale[g] (v / v_scale[g]), ties to the even
+ * code, magnitudes beyond the largest finite value saturating to it (448 or
+ * 127), and written to slot pos[b]; attention uses that rounded entry. The
+ * other arguments, the cache contract and the errors are those of
+ * fasttps_decode_step; in addition FASTTPS_ERR_INVALID_ARG for an unknown
+ * format or a scale that is not positive and finite. */
+FASTTPS_API int fasttps_decode_step_kv8(fasttps_layer* layer, const fasttps_weights* w, const void* x,
+                            const int32_t* pos, int32_t batch, int32_t kv_format, void* k_cache,
+                            void* v_cache, const float* k_scale, const float* v_scale, void* y,
+                            void* stream);
+
 /* The op-by-op baseline: the same step computed the way the paper's
  * standard implementation does it (Alg. 1: RoPE, Transpose, Concat, QK^T,
  * Softmax, PV; Alg. 2: gate, SiLU, up, elementwise mul, down; RMSNorm, the

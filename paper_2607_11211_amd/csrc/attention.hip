@@ -27,6 +27,12 @@
 //     keeps an online-softmax state (m, l, o-quarter) per query head;
 //   * the block merges its lanes' states (DPP within each 16-lane row, then
 //     the 16 rows through LDS) and writes (m, l, o) for its split.
+// The same kernel also serves an 8-bit cache (FP8 E4M3 or INT8 codes, one
+// scale per KV head for K and for V): a lane then loads d/4 bytes of a row,
+// decodes them with the hardware FP8 converts (or sign-extending byte
+// extracts), and the scales are folded into the softmax scale (K) and the
+// split's output (V); the new entry is rounded onto the 8-bit grid once, in
+// double precision, before it is stored and used.
 // A second small kernel combines the splits of each (b, head) with the
 // log-sum-exp identity. (Cross-block tickets are avoided on purpose: on this
 // chip an agent-scope fence per block costs far more than a kernel boundary.)
@@ -34,6 +40,8 @@
 #include "kernels.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace fasttps {
 
@@ -45,11 +53,31 @@ constexpr int kMaxSplits = 256;   // splits per (sequence, kv head); one combine
 
 constexpr int kRows = kThreads / 16;  // 16-lane DPP rows per block (4 positions each)
 
-template <int D, int G>
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+
+// bytes per cache element
+template <int KVF>
+constexpr int kv_bytes() { return KVF == kKvBf16 ? 2 : 1; }
+
+// A lane's quarter of one cache row: D / 4 elements in NC chunks of CB bytes
+// (16-byte chunks where the quarter allows, else 8-byte ones: a d = 96 row of
+// 8-bit codes gives 24 bytes per lane).
+template <int D, int KVF>
+struct LaneRow {
+  static constexpr int BYTES = D / 4 * kv_bytes<KVF>();
+  static constexpr int CB = BYTES % 16 == 0 ? 16 : 8;
+  static constexpr int NC = BYTES / CB;
+  static constexpr int EPC = CB / kv_bytes<KVF>();        // elements per chunk
+  static constexpr int ROW_CHUNKS = D * kv_bytes<KVF>() / CB;
+  typedef typename std::conditional<CB == 16, v4u, v2u>::type Chunk;
+};
+
+template <int D, int G, int KVF>
 struct alignas(16) AttnSmem {
   float q[G][D];
-  uint16_t knew[D];
-  uint16_t vnew[D];
+  alignas(16) uint8_t knew[D * kv_bytes<KVF>()];  // the new entry as stored
+  alignas(16) uint8_t vnew[D * kv_bytes<KVF>()];
   float red[G][kRows][D];  // the rows' o sums
   float rm[G][kRows];      // the rows' running max and sum
   float rl[G][kRows];
@@ -59,15 +87,83 @@ __device__ __forceinline__ float merge_factor(float m, float M) {
   return (m == -INFINITY) ? 0.f : __expf(m - M);
 }
 
+// four codes of one 32-bit word, element 4i + k in byte k
+template <int KVF>
+__device__ __forceinline__ void decode_word(uint32_t w, float* f) {
+  if constexpr (KVF == kKvFp8) {
+    const v2f lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+    const v2f hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+    f[0] = lo.x; f[1] = lo.y; f[2] = hi.x; f[3] = hi.y;
+  } else {
+    f[0] = (float)((int)(w << 24) >> 24);
+    f[1] = (float)((int)(w << 16) >> 24);
+    f[2] = (float)((int)(w << 8) >> 24);
+    f[3] = (float)((int)w >> 24);
+  }
+}
+
+// the EPC elements of one chunk as floats (unscaled codes for 8-bit caches)
+template <int KVF>
+__device__ __forceinline__ void decode_chunk(const v4u c, float* f) {
+  if constexpr (KVF == kKvBf16) {
+    unpack8(c, f);
+  } else {
+    decode_word<KVF>(c.x, f); decode_word<KVF>(c.y, f + 4);
+    decode_word<KVF>(c.z, f + 8); decode_word<KVF>(c.w, f + 12);
+  }
+}
+template <int KVF>
+__device__ __forceinline__ void decode_chunk(const v2u c, float* f) {
+  static_assert(KVF != kKvBf16, "bf16 rows use 16-byte chunks");
+  decode_word<KVF>(c.x, f); decode_word<KVF>(c.y, f + 4);
+}
+
+// The E4M3 code (OCP: bias 7, subnormals, largest finite 448) of a double:
+// nearest value, ties to the even code, magnitudes from 448 up saturating;
+// the sign bit is the sign of x. The quantum is 2^(e - 3) in the binade
+// [2^e, 2^(e+1)), e >= -6, and 2^-9 below (subnormals).
+__device__ __forceinline__ uint8_t f64_to_e4m3(double x) {
+  const uint32_t sign = signbit(x) ? 0x80u : 0u;
+  const double ax = fabs(x);
+  if (!(ax < 448.0)) return (uint8_t)(sign | 0x7Eu);
+  if (ax == 0.0) return (uint8_t)sign;
+  const int lead = ilogb(ax);                   // ax in [2^lead, 2^(lead+1))
+  const int qe = (lead < -6 ? -6 : lead) - 3;
+  const int q = (int)rint(ldexp(ax, -qe));      // nearest even; 0 .. 16
+  if (lead < -6) return (uint8_t)(sign | (uint32_t)q);  // subnormal, or 8 = 2^-6
+  const int e = q == 16 ? lead + 1 : lead;
+  const int m = q == 16 ? 0 : q - 8;
+  return (uint8_t)(sign | (uint32_t)((e + 7) << 3) | (uint32_t)m);
+}
+
+// The INT8 code of a double: nearest integer (ties to even), clamped to
+// [-127, 127], as its two's-complement byte.
+__device__ __forceinline__ uint8_t f64_to_int8(double x) {
+  const double r = fmin(fmax(rint(x), -127.0), 127.0);
+  return (uint8_t)(int8_t)(int)r;
+}
+
+// element e of the new entry, stored into the LDS row: bf16 of x, or the
+// 8-bit code of x / s
+template <int KVF>
+__device__ __forceinline__ void store_new(uint8_t* row, int e, double x, double s) {
+  if constexpr (KVF == kKvBf16) {
+    reinterpret_cast<uint16_t*>(row)[e] = f64_to_bf16(x);
+  } else if constexpr (KVF == kKvFp8) {
+    row[e] = f64_to_e4m3(x / s);
+  } else {
+    row[e] = f64_to_int8(x / s);
+  }
+}
+
 // This lane's K and V chunks of the tile at t0: position t0 + j (clamped to
-// `last`, a position of this split), quarter `seg` of d.
-template <int D>
-__device__ __forceinline__ void tile_load(v4u (&k)[D / 32], v4u (&v)[D / 32], const v4u* __restrict__ Kc,
-                                          const v4u* __restrict__ Vc, int t0, int last, int j, int seg) {
-  constexpr int C8 = D / 8, CH = D / 32;
-  const size_t base = (size_t)min(t0 + j, last) * C8 + seg * CH;
+// `last`, a position of this split), quarter `seg` of the row.
+template <int ROW_CHUNKS, int NC, typename Chunk>
+__device__ __forceinline__ void tile_load(Chunk (&k)[NC], Chunk (&v)[NC], const Chunk* __restrict__ Kc,
+                                          const Chunk* __restrict__ Vc, int t0, int last, int j, int seg) {
+  const size_t base = (size_t)min(t0 + j, last) * ROW_CHUNKS + seg * NC;
 #pragma unroll
-  for (int c = 0; c < CH; ++c) {
+  for (int c = 0; c < NC; ++c) {
     k[c] = Kc[base + c];
     v[c] = Vc[base + c];
   }
@@ -76,14 +172,18 @@ __device__ __forceinline__ void tile_load(v4u (&k)[D / 32], v4u (&v)[D / 32], co
 // PBF16: the softmax weights enter PV rounded to bf16, as FlashAttention's
 // bf16 P does (the row sum l keeps the fp32 weights); the accuracy study
 // compares this with the fp32 path. The step itself uses PBF16 = false.
-template <int D, int G, int NRING, bool PBF16>
-__global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
+// KVF: the cache's element format; kscale and vscale are the KV head's scales
+// of an 8-bit cache (unused for bf16).
+template <int D, int G, int NRING, bool PBF16, int KVF>
+__device__ __forceinline__ void attn_split_body(const AttnArgs& a, float kscale, float vscale) {
+  using R = LaneRow<D, KVF>;
+  using Chunk = typename R::Chunk;
   constexpr int SEG = D / 4;   // elements of a position row per lane
-  constexpr int CH = D / 32;   // 16-byte chunks per lane (K and V each)
-  constexpr int C8 = D / 8;    // 16-byte chunks per row
+  constexpr int NC = R::NC;    // chunks per lane (K and V each)
+  constexpr int RC = D * kv_bytes<KVF>() / 16;  // 16-byte chunks per row (the append)
   constexpr int HALF = D / 2;
-  static_assert(SEG % 8 == 0, "a lane's quarter row must be whole 16-byte chunks");
-  __shared__ AttnSmem<D, G> sm;
+  static_assert(SEG == NC * R::EPC, "a lane's quarter row must be whole chunks");
+  __shared__ AttnSmem<D, G, KVF> sm;
 
   const int tid = threadIdx.x;
   const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -93,9 +193,9 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   const int end = min(start + a.split_len, ntot);
   const int last = max(end - 1, start);  // a cache row of this split (start < N_max)
   const int H = a.n_heads, Hkv = a.n_kv_heads;
-  const size_t head_off = ((size_t)b * Hkv + g) * (size_t)a.max_seq * D;
-  const v4u* Kc = reinterpret_cast<const v4u*>(a.k_cache + head_off);
-  const v4u* Vc = reinterpret_cast<const v4u*>(a.v_cache + head_off);
+  const size_t head_off = ((size_t)b * Hkv + g) * (size_t)a.max_seq * D * kv_bytes<KVF>();  // bytes
+  const Chunk* Kc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.k_cache) + head_off);
+  const Chunk* Vc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.v_cache) + head_off);
   const int j = tid >> 2, seg = tid & 3;
 
   // ---- prologue operands first (every thread loads; clamped) ---------------
@@ -117,9 +217,9 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   __builtin_amdgcn_sched_barrier(0);  // keep the prologue loads ahead of the tiles
 
   // ---- the ring's first NRING tiles ------------------------------------------
-  v4u kr[NRING][CH], vr[NRING][CH];
+  Chunk kr[NRING][NC], vr[NRING][NC];
 #pragma unroll
-  for (int r = 0; r < NRING; ++r) tile_load<D>(kr[r], vr[r], Kc, Vc, start + r * kTile, last, j, seg);
+  for (int r = 0; r < NRING; ++r) tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, start + r * kTile, last, j, seg);
 
   // ---- prologue: RoPE in double, rounding of the new K/V --------------------
   if (tid < G * HALF) {
@@ -127,17 +227,23 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
     sm.q[ph][pj + HALF] = (float)((double)q1 * c_j + (double)q0 * s_j);
   }
   if (tid < HALF) {
-    sm.knew[pj] = f64_to_bf16((double)k0 * c_j - (double)k1 * s_j);
-    sm.knew[pj + HALF] = f64_to_bf16((double)k1 * c_j + (double)k0 * s_j);
+    store_new<KVF>(sm.knew, pj, (double)k0 * c_j - (double)k1 * s_j, (double)kscale);
+    store_new<KVF>(sm.knew, pj + HALF, (double)k1 * c_j + (double)k0 * s_j, (double)kscale);
   }
-  if (tid < D) sm.vnew[tid] = f32_to_bf16(v0);
+  if (tid < D) {
+    if constexpr (KVF == kKvBf16)
+      reinterpret_cast<uint16_t*>(sm.vnew)[tid] = f32_to_bf16(v0);
+    else
+      store_new<KVF>(sm.vnew, tid, (double)v0, (double)vscale);
+  }
   __syncthreads();
   // GKVC append (Eq. 1): the one cache write of the step
-  if (own_new && tid < 2 * C8) {
-    const bool isv = tid >= C8;
-    const int c = isv ? tid - C8 : tid;
+  if (own_new && tid < 2 * RC) {
+    const bool isv = tid >= RC;
+    const int c = isv ? tid - RC : tid;
     const v4u val = reinterpret_cast<const v4u*>(isv ? sm.vnew : sm.knew)[c];
-    uint16_t* dst = (isv ? a.v_cache : a.k_cache) + head_off + (size_t)P * D;
+    uint8_t* dst = static_cast<uint8_t*>(isv ? a.v_cache : a.k_cache) + head_off +
+                   (size_t)P * D * kv_bytes<KVF>();
     reinterpret_cast<v4u*>(dst)[c] = val;
   }
   // this lane's quarter of the query heads: registers for one head, LDS
@@ -157,7 +263,8 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < SEG; ++e) o[h][e] = 0.f;
   }
-  const float scale = a.scale;
+  // an 8-bit cache's K scale folds into the softmax scale
+  const float scale = KVF == kKvBf16 ? a.scale : a.scale * kscale;
   const int cend = min(end, P);  // slot P holds the new entry, handled below
   // one step of the online softmax with key kf and value vf
   auto update = [&](const float (&kf)[SEG], const float (&vf)[SEG], bool valid) {
@@ -185,15 +292,15 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
       const int tt = t0 + r * kTile;
       float kf[SEG], vf[SEG];
 #pragma unroll
-      for (int c = 0; c < CH; ++c) {
-        unpack8(kr[r][c], kf + 8 * c);
-        unpack8(vr[r][c], vf + 8 * c);
+      for (int c = 0; c < NC; ++c) {
+        decode_chunk<KVF>(kr[r][c], kf + R::EPC * c);
+        decode_chunk<KVF>(vr[r][c], vf + R::EPC * c);
       }
       // refill the slot with the tile NRING further on (clamped past the end);
       // the barrier keeps the refill after the unpack, so the new tile lands
       // in the registers the old one leaves (no copies, no early waits)
       __builtin_amdgcn_sched_barrier(0);
-      tile_load<D>(kr[r], vr[r], Kc, Vc, tt + NRING * kTile, last, j, seg);
+      tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, tt + NRING * kTile, last, j, seg);
       update(kf, vf, tt + j < cend);
     }
   }
@@ -202,9 +309,9 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   if (own_new && j == 0) {
     float kf[SEG], vf[SEG];
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      unpack8(reinterpret_cast<const v4u*>(sm.knew)[seg * CH + c], kf + 8 * c);
-      unpack8(reinterpret_cast<const v4u*>(sm.vnew)[seg * CH + c], vf + 8 * c);
+    for (int c = 0; c < NC; ++c) {
+      decode_chunk<KVF>(reinterpret_cast<const Chunk*>(sm.knew)[seg * NC + c], kf + R::EPC * c);
+      decode_chunk<KVF>(reinterpret_cast<const Chunk*>(sm.vnew)[seg * NC + c], vf + R::EPC * c);
     }
     update(kf, vf, true);
   }
@@ -247,12 +354,23 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
       O = fmaf(sm.red[h][r][e], f, O);
     }
     float* pr = part_b + ((size_t)(g * G + h) * a.nsplit_cap + s) * (D + 2);
-    pr[2 + e] = O;
+    pr[2 + e] = KVF == kKvBf16 ? O : O * vscale;  // an 8-bit cache's V scale
     if (e == 0) {
       pr[0] = M;
       pr[1] = L;
     }
   }
+}
+
+template <int D, int G, int NRING, bool PBF16>
+__global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
+  attn_split_body<D, G, NRING, PBF16, kKvBf16>(a, 1.f, 1.f);
+}
+
+// 8-bit cache: the KV head's two scales come from the argument block
+template <int D, int G, int KVF>
+__global__ __launch_bounds__(kThreads) void attn_split_kv8_kernel(AttnArgs a, KvScales sc) {
+  attn_split_body<D, G, 1, false, KVF>(a, sc.k[blockIdx.y], sc.v[blockIdx.y]);
 }
 
 // o[b, h] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s,  M = max_s m_s.
@@ -322,6 +440,26 @@ hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   return ext_launch(attn_split_kernel<D, G, NRING, false>, grid, dim3(kThreads), 0, s, ev, a);
 }
 
+template <int D, int G>
+hipError_t launch_kv8_dg(const AttnArgs& a, const KvScales& sc, hipStream_t s, KernelEvents ev) {
+  dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
+  switch (a.kv_format) {
+    case kKvFp8: return ext_launch(attn_split_kv8_kernel<D, G, kKvFp8>, grid, dim3(kThreads), 0, s, ev, a, sc);
+    case kKvInt8: return ext_launch(attn_split_kv8_kernel<D, G, kKvInt8>, grid, dim3(kThreads), 0, s, ev, a, sc);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int D>
+hipError_t launch_kv8_d(const AttnArgs& a, const KvScales& sc, hipStream_t s, KernelEvents ev) {
+  switch (a.n_heads / a.n_kv_heads) {
+    case 1: return launch_kv8_dg<D, 1>(a, sc, s, ev);
+    case 2: return launch_kv8_dg<D, 2>(a, sc, s, ev);
+    case 4: return launch_kv8_dg<D, 4>(a, sc, s, ev);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int D>
 hipError_t launch_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   switch (a.n_heads / a.n_kv_heads) {
@@ -347,6 +485,17 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
     case 64: return launch_d<64>(a, s, ev);
     case 96: return launch_d<96>(a, s, ev);
     case 128: return launch_d<128>(a, s, ev);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_attention_kv8(const AttnArgs& a, const KvScales& sc, hipStream_t s, KernelEvents ev) {
+  if (a.nsplit < 1 || a.nsplit > a.nsplit_cap || a.nsplit > kMaxSplits) return hipErrorInvalidValue;
+  if (a.n_kv_heads > kMaxKvHeads) return hipErrorInvalidValue;
+  switch (a.head_dim) {
+    case 64: return launch_kv8_d<64>(a, sc, s, ev);
+    case 96: return launch_kv8_d<96>(a, sc, s, ev);
+    case 128: return launch_kv8_d<128>(a, sc, s, ev);
     default: return hipErrorInvalidValue;
   }
 }

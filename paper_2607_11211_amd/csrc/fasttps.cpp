@@ -396,7 +396,7 @@ namespace {
 // The checks shared by both step entry points; on success *maxp is the largest
 // position of the batch. Makes no HIP call.
 int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
-               void* k_cache, void* v_cache, void* y, int* maxp) {
+               void* k_cache, void* v_cache, void* y, int* maxp, size_t cache_elem_bytes = 2) {
   if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
   if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad weights handle");
   const fasttps_config& c = l->cfg;
@@ -415,7 +415,7 @@ int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const 
   }
   const size_t D = c.hidden, d = c.head_dim;
   const size_t act_bytes = (size_t)batch * D * 2;
-  const size_t cache_bytes = (size_t)batch * c.n_kv_heads * c.max_seq * d * 2;
+  const size_t cache_bytes = (size_t)batch * c.n_kv_heads * c.max_seq * d * cache_elem_bytes;
   if (overlaps(y, act_bytes, x, act_bytes) || overlaps(y, act_bytes, k_cache, cache_bytes) ||
       overlaps(y, act_bytes, v_cache, cache_bytes))
     return fail(FASTTPS_ERR_INVALID_ARG, "y overlaps x or a cache");
@@ -427,12 +427,14 @@ int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const 
 
 }  // namespace
 
-int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
-                        int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
-  g_last_error.clear();
-  int maxp = 0;
-  const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
-  if (st) return st;
+}  // extern "C"
+
+namespace {
+
+// The fused step after validation: kvf is the cache format (kKvBf16, or an
+// 8-bit format with its scales in *sc).
+int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
+             void* k_cache, void* v_cache, void* y, void* stream, int maxp, int kvf, const KvScales* sc) {
   const fasttps_config& c = l->cfg;
   const size_t D = c.hidden, d = c.head_dim;
 
@@ -489,8 +491,10 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   aa.nsplit_cap = l->nsplit_cap;
   aa.scale = (float)(1.0 / std::sqrt((double)d));
   aa.p_bf16 = l->p_bf16;
+  aa.kv_format = kvf;
   for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
-  if ((e = launch_attention(aa, s, ev[1])) != hipSuccess) return hip_fail(e, "attention launch");
+  e = kvf == kKvBf16 ? launch_attention(aa, s, ev[1]) : launch_attention_kv8(aa, *sc, s, ev[1]);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
   if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
 
   GemvArgs oa{};
@@ -527,6 +531,43 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   if ((e = launch_down_residual(da, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
   if (timed) ++l->prof_n;
   return FASTTPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
+                        int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
+  g_last_error.clear();
+  int maxp = 0;
+  const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
+  if (st) return st;
+  return run_step(l, w, x, pos, batch, k_cache, v_cache, y, stream, maxp, kKvBf16, nullptr);
+}
+
+int fasttps_decode_step_kv8(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
+                            int32_t batch, int32_t kv_format, void* k_cache, void* v_cache, const float* k_scale,
+                            const float* v_scale, void* y, void* stream) {
+  g_last_error.clear();
+  if (kv_format != FASTTPS_KV_FP8_E4M3 && kv_format != FASTTPS_KV_INT8)
+    return fail(FASTTPS_ERR_INVALID_ARG, "unknown KV format %d", kv_format);
+  int maxp = 0;
+  const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp, 1);
+  if (st) return st;
+  if (!k_scale || !v_scale) return fail(FASTTPS_ERR_INVALID_ARG, "null scale array");
+  const int Hkv = l->cfg.n_kv_heads;
+  if (Hkv > kMaxKvHeads) return fail(FASTTPS_ERR_UNSUPPORTED, "n_kv_heads %d > %d", Hkv, kMaxKvHeads);
+  KvScales sc{};
+  for (int g = 0; g < Hkv; ++g) {
+    if (!(std::isfinite(k_scale[g]) && k_scale[g] > 0.f) || !(std::isfinite(v_scale[g]) && v_scale[g] > 0.f))
+      return fail(FASTTPS_ERR_INVALID_ARG, "KV head %d: scales must be positive and finite", g);
+    sc.k[g] = k_scale[g];
+    sc.v[g] = v_scale[g];
+  }
+  static_assert(FASTTPS_KV_FP8_E4M3 == kKvFp8 && FASTTPS_KV_INT8 == kKvInt8, "format codes");
+  const int kvf = kv_format;
+  return run_step(l, w, x, pos, batch, k_cache, v_cache, y, stream, maxp, kvf, &sc);
 }
 
 int fasttps_debug_read(fasttps_layer* l, int32_t which, int32_t batch, void* dst, size_t bytes, void* stream) {

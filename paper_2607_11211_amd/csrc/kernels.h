@@ -60,18 +60,29 @@ struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
   const double* rope_cos;  // [N_max, d/2]
   const double* rope_sin;  // [N_max, d/2]
-  uint16_t* k_cache;       // [B, H_kv, N_max, d]
-  uint16_t* v_cache;
+  void* k_cache;           // [B, H_kv, N_max, d], bf16 or 8-bit codes
+  void* v_cache;
   float* part;             // [batch, H, nsplit_cap, d + 2] split partials (m, l, o)
   float* o;                // [batch, H d] fp32
   int batch, n_heads, n_kv_heads, head_dim, max_seq;
   int split_len, nsplit, nsplit_cap;
   float scale;             // 1/sqrt(d)
   int p_bf16;              // accuracy study: softmax weights rounded to bf16 before PV
+  int kv_format;           // kKvBf16, kKvFp8 or kKvInt8
   PosArray pos;
+};
+// cache element formats (the values of the ABI's FASTTPS_KV_* constants)
+constexpr int kKvBf16 = 0, kKvFp8 = 1, kKvInt8 = 2;
+constexpr int kMaxKvHeads = 128;  // n_heads * head_dim <= 8192, head_dim >= 64
+// the per-KV-head scales of an 8-bit cache, passed by value
+struct KvScales {
+  float k[kMaxKvHeads];
+  float v[kMaxKvHeads];
 };
 // per split: RoPE, append, partial softmax state (m, l, o)
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
+// the same over an 8-bit cache (a.kv_format kKvFp8 or kKvInt8)
+hipError_t launch_attention_kv8(const AttnArgs& a, const KvScales& sc, hipStream_t s, KernelEvents ev = {});
 // combine the split partials into o
 hipError_t launch_attention_combine(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
 

@@ -27,10 +27,14 @@ ERR_BAD_HANDLE = -7
 
 DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
 
+KV_FP8_E4M3 = 1
+KV_INT8 = 2
+KV_FORMATS = {"fp8_e4m3": KV_FP8_E4M3, "int8": KV_INT8}
+
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
-           "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
+           "fasttps_decode_step_kv8", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 6
 
 
@@ -62,6 +66,8 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_weights_pack.argtypes = [vp, ctypes.POINTER(WeightsDesc), vp, ctypes.POINTER(vp)]
     lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     lib.fasttps_decode_step_unfused.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
+    fp = ctypes.POINTER(ctypes.c_float)
+    lib.fasttps_decode_step_kv8.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, i32, vp, vp, fp, fp, vp, vp]
     lib.fasttps_unfused_enable.argtypes = [vp]
     lib.fasttps_set_attention_p_bf16.argtypes = [vp, i32]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
@@ -78,7 +84,7 @@ def _load() -> ctypes.CDLL:
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
                  "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
-                 "fasttps_set_attention_p_bf16"):
+                 "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -160,6 +166,28 @@ class Layer:
                                        p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
                                        _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step")
+
+    def step_kv8(self, weights: Weights, fmt: str, x, pos, k_cache, v_cache, k_scale, v_scale, y,
+                 stream=None) -> None:
+        """Enqueue one decode step over an 8-bit cache (fmt "fp8_e4m3" or "int8").
+
+        k_cache, v_cache: uint8 device tensors [batch, H_kv, N_max, d] of codes;
+        k_scale, v_scale: host float sequences [H_kv], the per-KV-head scales.
+        """
+        if fmt not in KV_FORMATS:
+            raise ValueError(f"unknown 8-bit KV format {fmt!r}")
+        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
+        ks = np.ascontiguousarray(np.asarray(k_scale, dtype=np.float32))
+        vs = np.ascontiguousarray(np.asarray(v_scale, dtype=np.float32))
+        if ks.shape != (self.cfg.n_kv_heads,) or vs.shape != (self.cfg.n_kv_heads,):
+            raise ValueError(f"scales must have shape ({self.cfg.n_kv_heads},)")
+        fptr = ctypes.POINTER(ctypes.c_float)
+        _check(LIB.fasttps_decode_step_kv8(self.handle, weights.handle, _ptr(x),
+                                           p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(p.shape[0]),
+                                           KV_FORMATS[fmt], _ptr(k_cache), _ptr(v_cache),
+                                           ks.ctypes.data_as(fptr), vs.ctypes.data_as(fptr), _ptr(y),
+                                           _stream_handle(stream)),
+               "fasttps_decode_step_kv8")
 
     def enable_unfused(self) -> None:
         """Allocate the op-by-op baseline's scratch (once per handle)."""

@@ -34,9 +34,10 @@ def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
     return np.abs(key(a_bits) - key(b_bits))
 
 
-def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=False):
+def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=False, kv8=None):
     """One decode step on cuda:0 through the C ABI (the op-by-op baseline when
-    unfused). Returns host copies."""
+    unfused; over an 8-bit cache when kv8 = (fmt, k_codes, v_codes, k_scale,
+    v_scale)). Returns host copies."""
     import torch
     from paper_2607_11211_amd import layer as L
     lay = layer if layer is not None else L.Layer(cfg)
@@ -46,11 +47,17 @@ def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=
         W = lay.pack(wt)
         del wt
     x = L.to_device(inp.x)
-    kc = L.to_device(inp.k_cache)
-    vc = L.to_device(inp.v_cache)
+    if kv8 is not None:
+        kc = torch.from_numpy(np.ascontiguousarray(kv8[1])).to(x.device)
+        vc = torch.from_numpy(np.ascontiguousarray(kv8[2])).to(x.device)
+    else:
+        kc = L.to_device(inp.k_cache)
+        vc = L.to_device(inp.v_cache)
     y = torch.empty_like(x)
     B = cfg.batch
-    if unfused:
+    if kv8 is not None:
+        lay.step_kv8(W, kv8[0], x, inp.pos, kc, vc, kv8[3], kv8[4], y)
+    elif unfused:
         lay.enable_unfused()
         lay.step_unfused(W, x, inp.pos, kc, vc, y)
         debug = False
@@ -66,7 +73,10 @@ def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=
             lay.debug_read(which, B, t)
             out[name] = t
     torch.cuda.synchronize()
-    res = {"y": L.from_device(y), "k_cache": L.from_device(kc), "v_cache": L.from_device(vc)}
+    if kv8 is not None:
+        res = {"y": L.from_device(y), "k_cache": kc.cpu().numpy(), "v_cache": vc.cpu().numpy()}
+    else:
+        res = {"y": L.from_device(y), "k_cache": L.from_device(kc), "v_cache": L.from_device(vc)}
     for k, t in out.items():
         res[k] = t.cpu().numpy().astype(np.float64)
     if keep:

@@ -44,6 +44,17 @@ def test_unfused_entry_points_reject_bad_handles(L):
     assert L.LIB.fasttps_decode_step_unfused(None, None, None, p, 1, None, None, None, None) == L.ERR_BAD_HANDLE
 
 
+def test_kv8_entry_point_rejects_bad_format_and_handles(L):
+    p = (ctypes.c_int32 * 1)(0)
+    sc = (ctypes.c_float * 1)(1.0)
+    f = L.LIB.fasttps_decode_step_kv8
+    for fmt in (0, 3, -1):
+        assert f(None, None, None, p, 1, fmt, None, None, sc, sc, None, None) == L.ERR_INVALID_ARG
+        assert "format" in L.last_error()
+    for fmt in (L.KV_FP8_E4M3, L.KV_INT8):
+        assert f(None, None, None, p, 1, fmt, None, None, sc, sc, None, None) == L.ERR_BAD_HANDLE
+
+
 def test_probe_library_exports_its_header():
     """The measurement aid (stream-read probe) is a library of its own with
     its own header; it rejects bad arguments before touching the GPU."""

@@ -1,0 +1,186 @@
+"""Parity of the decode step over an 8-bit KV cache (FP8 E4M3 or INT8 codes,
+one scale per KV head) with the fp64 oracle, through the C ABI (MI355X).
+
+Bars:
+  * cache bytes outside the appended slots are unchanged (bit-exact);
+  * appended codes equal the oracle's, except where the exact value
+    k_rope / scale (v / scale) lies within the GPU's projection error
+    (QKV_TOL times the sequence's largest |k| or |v|, over the scale) of the
+    midpoint between the two codes: there floating point decides the integer
+    and either neighbour is a correct rounding of the GPU's own value;
+  * attention o, h1, the MLP activation and y meet the bars of the bf16 step,
+    against the oracle run on the GPU's appended codes (teacher forcing,
+    which changes nothing where the codes agree).
+"""
+import numpy as np
+import pytest
+
+from gpu_harness import QKV_TOL, check_intermediates, check_y, log, run_gpu
+from oracle import kvquant as kq
+from oracle import ref
+from paper_2607_11211_amd import configs, inputs
+from paper_2607_11211_amd.configs import LayerConfig
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_11211_amd.layer  # noqa: F401  (fails loudly if the library is missing)
+
+
+SMALL = [
+    LayerConfig(name="k8_gqa64", index=40, batch=6, hidden=512, n_heads=8, n_kv_heads=2, head_dim=64,
+                intermediate=1376, rope_base=10000.0, max_seq=384, pos=(0, 1, 63, 64, 65, 300)),
+    LayerConfig(name="k8_mha96", index=41, batch=3, hidden=768, n_heads=8, n_kv_heads=8, head_dim=96,
+                intermediate=2048, rope_base=10000.0, max_seq=256, pos=(127, 200, 255)),
+    LayerConfig(name="k8_gqa128", index=42, batch=3, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
+                intermediate=2824, rope_base=500000.0, max_seq=1100, pos=(5, 511, 1000)),
+    LayerConfig(name="k8_g2_b9", index=43, batch=9, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=200, pos=(0, 3, 17, 64, 100, 128, 150, 190, 199)),
+]
+
+
+def make_kv8(cfg, inp, fmt, layer=0):
+    kc = inputs.make_cache8(cfg, inp.pos, "k", fmt, layer)
+    vc = inputs.make_cache8(cfg, inp.pos, "v", fmt, layer)
+    ks = inputs.make_kv_scales(cfg, "k", fmt, layer)
+    vs = inputs.make_kv_scales(cfg, "v", fmt, layer)
+    return kc, vc, ks, vs
+
+
+def check_codes(cfg, inp, fmt, orig, got, exact, scale, want_codes, name):
+    """Untouched bytes bit-exact; appended codes as the module header says. Returns the mismatch count."""
+    B, G, d = cfg.batch, cfg.n_kv_heads, cfg.head_dim
+    slot = np.empty((B, G, d), np.uint8)
+    masked = got.copy()
+    for b in range(B):
+        p = int(inp.pos[b])
+        slot[b] = got[b, :, p, :]
+        masked[b, :, p, :] = orig[b, :, p, :]
+    assert np.array_equal(masked, orig), f"{name}-cache bytes outside the appended slots changed"
+    sc = np.asarray(scale, np.float64)[None, :, None]
+    x = exact / sc                                         # exact scaled values
+    lim = kq.E4M3_MAX if fmt == kq.FP8_E4M3 else kq.INT8_MAX
+    xc = np.clip(x, -lim, lim)
+    vg = kq.code_values(slot, fmt)
+    vo = kq.code_values(want_codes, fmt)
+    assert np.all(np.isfinite(vg)), f"appended {name} holds NaN codes"
+    if fmt == kq.INT8:
+        assert not np.any(slot == 0x80), f"appended {name} uses -128"
+    diff = vg != vo
+    if diff.any():
+        # GPU error bound on the scaled value: QKV_TOL of the sequence's largest |value|, over the scale
+        tol = QKV_TOL * np.max(np.abs(exact), axis=(1, 2), keepdims=True) / sc
+        tol = np.broadcast_to(tol, x.shape)
+        mid = (vg + vo) / 2.0
+        ok = np.abs(xc - mid) <= tol
+        assert np.all(ok[diff]), (f"appended {name}: {int(np.sum(diff & ~ok))} codes differ from the oracle "
+                                  f"away from a rounding boundary")
+    return int(diff.sum())
+
+
+def run_case(cfg, inp, fmt, layer=None, weights=None):
+    kc, vc, ks, vs = make_kv8(cfg, inp, fmt)
+    kv = kq.KvQuant(fmt, tuple(float(v) for v in ks), tuple(float(v) for v in vs))
+    W = ref.widen_weights(inp.weights)
+    r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, kc, vc, W, kv=kv)
+    gpu = run_gpu(cfg, inp, layer=layer, weights=weights, kv8=(fmt, kc, vc, ks, vs))
+    B, G = cfg.batch, cfg.n_kv_heads
+    gk = np.stack([gpu["k_cache"][b, :, int(inp.pos[b]), :] for b in range(B)])
+    gv = np.stack([gpu["v_cache"][b, :, int(inp.pos[b]), :] for b in range(B)])
+    mk = check_codes(cfg, inp, fmt, kc, gpu["k_cache"], r["k_rope"], ks, r["k_new_bits"], "k")
+    mv = check_codes(cfg, inp, fmt, vc, gpu["v_cache"], r["v"], vs, r["v_new_bits"], "v")
+    r_tf = r if (mk == 0 and mv == 0) else ref.decode_layer_cfg(cfg, inp.x, inp.pos, kc, vc, W, kv=kv,
+                                                                new_entries=(gk, gv))
+    yerr = check_y(gpu, r_tf)
+    worst = check_intermediates(cfg, inp, gpu, r_tf)
+    log(f"{cfg.name} {fmt}: pos={inp.pos.tolist()[:8]} code mismatches k {mk} v {mv} of {B * G * cfg.head_dim} "
+        f"each; y_err={yerr:.2e} inter={worst}")
+    return gpu, r_tf
+
+
+@pytest.mark.parametrize("fmt", kq.FORMATS)
+@pytest.mark.parametrize("cfg", SMALL, ids=lambda c: c.name)
+def test_kv8_small_shapes(cfg, fmt):
+    log(f"start {cfg.name} {fmt}")
+    run_case(cfg, inputs.make_layer_inputs(cfg), fmt)
+
+
+@pytest.mark.parametrize("name,fmt", [("tiny", "int8"), ("phi3_kv1k", "fp8_e4m3"), ("phi3_kv4k", "fp8_e4m3"),
+                                      ("phi3_kv4k", "int8"), ("gqa_longctx", "fp8_e4m3"),
+                                      ("phi3_batch16_ragged", "int8")])
+def test_kv8_workloads(name, fmt):
+    cfg = configs.get(name)
+    log(f"start {name} {fmt}")
+    inp = inputs.make_layer_inputs(cfg)
+    run_case(cfg.with_pos(inp.pos), inp, fmt)
+
+
+@pytest.mark.parametrize("fmt", kq.FORMATS)
+def test_kv8_consecutive_steps(fmt):
+    """Three tokens in a row on one 8-bit cache: each step reads the codes the
+    previous ones appended."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    cfg = LayerConfig(name="k8_steps", index=44, batch=2, hidden=512, n_heads=8, n_kv_heads=2, head_dim=64,
+                      intermediate=1376, rope_base=10000.0, max_seq=160, pos=(62, 127))
+    inp = inputs.make_layer_inputs(cfg)
+    kc, vc, ks, vs = make_kv8(cfg, inp, fmt)
+    kv = kq.KvQuant(fmt, tuple(float(v) for v in ks), tuple(float(v) for v in vs))
+    lay = L.Layer(cfg)
+    Wd = lay.pack({k: L.to_device(v) for k, v in inp.weights.items()})
+    W = ref.widen_weights(inp.weights)
+    dk = torch.from_numpy(kc.copy()).cuda()
+    dv = torch.from_numpy(vc.copy()).cuda()
+    pos = inp.pos.copy()
+    host_k, host_v = kc.copy(), vc.copy()
+    try:
+        for step in range(3):
+            x_bits = inputs.make_x(cfg, seed=200 + step)
+            x = L.to_device(x_bits)
+            y = torch.empty_like(x)
+            lay.step_kv8(Wd, fmt, x, pos, dk, dv, ks, vs, y)
+            torch.cuda.synchronize()
+            gk, gv = dk.cpu().numpy(), dv.cpu().numpy()
+            r = ref.decode_layer_cfg(cfg, x_bits, pos, host_k, host_v, W, kv=kv)
+            sk = np.stack([gk[b, :, int(pos[b]), :] for b in range(cfg.batch)])
+            sv = np.stack([gv[b, :, int(pos[b]), :] for b in range(cfg.batch)])
+            step_inp = inputs.LayerInputs(cfg=cfg, x=x_bits, pos=pos, weights=inp.weights, k_cache=host_k,
+                                          v_cache=host_v)
+            check_codes(cfg, step_inp, fmt, host_k, gk, r["k_rope"], ks, r["k_new_bits"], "k")
+            check_codes(cfg, step_inp, fmt, host_v, gv, r["v"], vs, r["v_new_bits"], "v")
+            r = ref.decode_layer_cfg(cfg, x_bits, pos, host_k, host_v, W, kv=kv, new_entries=(sk, sv))
+            check_y({"y": L.from_device(y)}, r)
+            host_k, host_v = gk, gv
+            pos = pos + 1
+    finally:
+        lay.destroy()
+
+
+def test_kv8_rejects_bad_scales_before_launch():
+    """Scales that are not positive and finite are refused on the host; the caches stay untouched."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    cfg = SMALL[0]
+    inp = inputs.make_layer_inputs(cfg)
+    kc, vc, ks, vs = make_kv8(cfg, inp, "fp8_e4m3")
+    lay = L.Layer(cfg)
+    try:
+        Wd = lay.pack({k: L.to_device(v) for k, v in inp.weights.items()})
+        dk, dv = torch.from_numpy(kc).cuda(), torch.from_numpy(vc).cuda()
+        x = L.to_device(inp.x)
+        y = torch.empty_like(x)
+        for bad in (0.0, -1.0, float("nan"), float("inf")):
+            ks2 = ks.copy()
+            ks2[-1] = bad
+            with pytest.raises(L.FastTPSError) as e:
+                lay.step_kv8(Wd, "fp8_e4m3", x, inp.pos, dk, dv, ks2, vs, y)
+            assert e.value.status == L.ERR_INVALID_ARG
+        torch.cuda.synchronize()
+        assert np.array_equal(dk.cpu().numpy(), kc) and np.array_equal(dv.cpu().numpy(), vc)
+    finally:
+        lay.destroy()
