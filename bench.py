@@ -34,6 +34,15 @@ if ROOT not in sys.path:
 PEAK_HBM_GBPS = 8000.0
 METRIC = "decode-step layer latency (µs) + achieved HBM GB/s vs peak, Phi-3-mini shape"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+ROTATE_BYTES = 2 << 30
+WORKLOAD_TEXT = {
+    "phi3_stack32_kv4k": "Phi-3-mini-shaped decoder stack, 32 layers, batch 1, KV length 4096 per layer, one decode step",
+    "phi3_kv1k": "Phi-3-mini-shaped layer, batch 1, KV length 1024",
+    "phi3_kv4k": "Phi-3-mini-shaped layer, batch 1, KV length 4096",
+    "phi3_batch16_ragged": "Phi-3-mini-shaped layer, 16 sequences, ragged KV lengths U[512, 4096]",
+    "gqa_longctx": "GQA layer (4096 hidden, 32/8 heads x 128, MLP 14336), 4 sequences, KV length 32768",
+    "tiny": "tiny layer (256 hidden, 4 x 64 heads, MLP 688), KV length 128",
+}
 
 
 def log(msg: str) -> None:
@@ -261,6 +270,8 @@ def main() -> int:
                          "one JSON line per point, instead of the benchmark")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip timing the op-by-op baseline (Alg. 1 + Alg. 2 operators, Concat reloading the cache)")
+    ap.add_argument("--gemm", choices=["auto", "vector", "matrix"], default="auto",
+                    help="projection kernels: vector GEMVs, MFMA (matrix cores), or the library's choice by batch")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="finish with a plain 256 MiB device copy (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -280,12 +291,17 @@ def main() -> int:
         return sweep(args)
     torch.cuda.set_device(0)
     cfg = configs.get(args.workload)
-    nl = cfg.layers
     pos = inputs.make_pos(cfg)
     cfg = cfg.with_pos(pos)
+    # a single-layer workload runs as a chain of independent copies (own
+    # weights and caches) totalling at least 2 GB, so that no copy is still
+    # in the 256 MB Infinity Cache when the chain comes back to it
+    nl = cfg.layers if cfg.layers > 1 else max(1, -(-ROTATE_BYTES // cfg.step_bytes(pos)))
     log(f"workload {cfg.name}: {nl} layers, batch {cfg.batch}, pos {pos.tolist()[:4]}")
 
-    lay = L.Layer(cfg)
+    gemm = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX}[args.gemm]
+    lay = L.Layer(cfg, max_batch=max(cfg.batch, 2) if args.gemm == "matrix" else None)
+    lay.set_gemm_path(gemm)
     weights, kcs, vcs = [], [], []
     gen = torch.Generator(device="cuda")
     gen.manual_seed(0xFA57 + cfg.index)
@@ -454,10 +470,11 @@ def main() -> int:
         "metric": METRIC, "value": round(us_layer, 3), "unit": "us", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": False,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage": "bf16", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: Phi-3-mini-shaped decoder stack, {nl} layers, batch {cfg.batch}, "
-                               f"KV length {int(pos[0])} per layer, one decode step",
+        "config": {"workload": f"{cfg.name}: {WORKLOAD_TEXT.get(cfg.name, cfg.name)}"
+                               + ("" if cfg.layers > 1 else f" ({nl} rotating copies)"),
                    "layers": nl, "global_batch": cfg.batch, "seq_len": int(pos.max()) + 1,
                    "parallelism": "single GPU"},
+        "gemm_path": args.gemm,
         "hbm_gbps": round(gbps, 1), "hbm_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "read_ceiling": {"gbps": round(ceiling, 1),
                          "method": f"libfasttps_probe stream read of 4 GiB with 16-byte loads, best launch "

@@ -172,6 +172,29 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
                                 const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
                                 void* y, void* stream);
 
+/* Which kernels run the four projections (QKV, O, gate/up, down).
+ *   FASTTPS_GEMM_VECTOR  weight-streaming GEMVs on the vector ALUs (fp32
+ *                        activations); the only path of a layer with
+ *                        max_batch == 1
+ *   FASTTPS_GEMM_MATRIX  weight-streaming MFMA kernels (bf16 weights times
+ *                        activations split into two bf16 levels, fp32
+ *                        accumulation); needs max_batch > 1, for which
+ *                        fasttps_weights_pack also stores the weights in the
+ *                        MFMA tile order (about twice the weight memory)
+ *   FASTTPS_GEMM_AUTO    (default) the matrix path from 2 sequences up where
+ *                        the weights carry the tiles, else the vector path
+ * At batch 8-16 the projections are dense enough that the multiply-adds
+ * outgrow the vector ALUs beside the weight stream (Section 4.4 puts the
+ * token-phase projections at the weight stream); both paths read every
+ * weight once per step. Returns FASTTPS_ERR_INVALID_ARG for an unknown path,
+ * or for FASTTPS_GEMM_MATRIX on a layer with max_batch == 1. A step with the
+ * matrix path and weights packed for max_batch == 1 fails with
+ * FASTTPS_ERR_INVALID_ARG before any launch. */
+#define FASTTPS_GEMM_AUTO 0
+#define FASTTPS_GEMM_VECTOR 1
+#define FASTTPS_GEMM_MATRIX 2
+FASTTPS_API int fasttps_set_gemm_path(fasttps_layer* layer, int32_t path);
+
 /* Accuracy-study hook: when enabled, later steps of this layer handle round
  * the softmax weights to bf16 before the PV accumulation, as FlashAttention
  * does with its bf16 P (the softmax row sum stays fp32), so the attention

@@ -384,7 +384,8 @@ constexpr int kCombineRegs = 16;  // splits per thread held in registers
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
                                                                        int nsplit_cap, int n_heads,
-                                                                       float* __restrict__ o) {
+                                                                       float* __restrict__ o,
+                                                                       uint16_t* __restrict__ o_operand, int o_nbtc) {
   constexpr int NG = kCombineThreads / D;  // thread groups over the splits
   __shared__ float fac[kMaxSplits];
   __shared__ float red[kCombineThreads / kWave];
@@ -426,7 +427,20 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
     float O = 0.f;
 #pragma unroll
     for (int g2 = 0; g2 < NG; ++g2) O += osum[g2][tid];
-    o[((size_t)b * n_heads + h) * D + tid] = O / L;
+    const float ov2 = O / L;
+    o[((size_t)b * n_heads + h) * D + tid] = ov2;
+    if (o_operand) {
+      // the MFMA O projection's operand: hi/lo bf16 split of o at input
+      // k = h D + tid, in the lane order of the A operand (row 2 (b % 8) +
+      // level, k-group (k / 8) % 4 of k-tile k / 32, batch tile b / 8)
+      const int k = h * D + tid;
+      const uint16_t hi = f32_to_bf16(ov2);
+      const uint16_t lo = f32_to_bf16(ov2 - bf16_to_f32(hi));
+      const size_t base = (((size_t)(k >> 5) * o_nbtc + b / 8) * kWave + 2 * (b % 8) + 16 * ((k >> 3) & 3)) * 8 +
+                          (k & 7);
+      o_operand[base] = hi;
+      o_operand[base + 8] = lo;
+    }
   }
 }
 
@@ -474,7 +488,7 @@ template <int D>
 hipError_t launch_combine_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(a.n_heads, a.batch);
   return ext_launch(attn_combine_kernel<D>, grid, dim3(kCombineThreads), 0, s, ev, (const float*)a.part, a.nsplit,
-                    a.nsplit_cap, a.n_heads, a.o);
+                    a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
 }
 
 }  // namespace

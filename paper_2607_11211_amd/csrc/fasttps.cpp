@@ -53,6 +53,44 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 int round_up(int v, int m) { return (v + m - 1) / m * m; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// Shapes of the MFMA-tiled matrices: stripes of rh output rows (gate/up:
+// rh / 2 units, i.e. rh / 2 gate and rh / 2 up rows) by k-tiles of 32 inputs.
+struct TileDims {
+  int ns, kt, rh;
+  size_t elems() const { return (size_t)ns * kt * 32 * rh; }
+};
+struct LayerTiles {
+  TileDims qkv, o, gu, down;
+};
+// The stripe height (16, 12 or 8 rows) that gives the most loaded of the
+// kMfmaBlocks blocks the fewest rows (units of `per_row` rows for gate/up),
+// the tallest on ties: 9216 rows go in 768 stripes of 12 (3 per block), 3072
+// in 256 of 12, 4096 in 256 of 16.
+constexpr int kMfmaBlocks = 256;
+TileDims pick_tiles(int rows, int din, int per_row) {
+  TileDims best{0, ceil_div(din, 32), 0};
+  long best_load = 0;
+  for (int rh : {16, 12, 8}) {
+    const int units = rh / per_row;
+    const int ns = ceil_div(rows, units);
+    const int g = std::min(ns, kMfmaBlocks);
+    const long load = (long)ceil_div(ns, g) * units;
+    if (best.rh == 0 || load < best_load) {
+      best = {ns, ceil_div(din, 32), rh};
+      best_load = load;
+    }
+  }
+  return best;
+}
+LayerTiles layer_tiles(const fasttps_config& c) {
+  const int D = c.hidden, K = c.intermediate, q = c.n_heads * c.head_dim;
+  const int rows_qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+  return {pick_tiles(rows_qkv, D, 1), pick_tiles(D, q, 1), pick_tiles(K, D, 2), pick_tiles(D, K, 1)};
+}
+// the MFMA path is taken from this batch size up (FASTTPS_GEMM_AUTO)
+constexpr int kMfmaMinBatch = 2;
+constexpr int kMfmaWaves = 16;  // waves per block of the MFMA kernels (they split the k-tiles)
+
 // Interlaced W_gu (Section 3.2 item 1, Alg. 4) in tiles of one row: packed
 // row 2k is W_gate row k, row 2k + 1 is W_up row k, so the gate/up pair of an
 // intermediate unit is one contiguous 2D-value row for the projection kernel.
@@ -74,6 +112,15 @@ struct fasttps_layer {
   float* attn_o;
   float* h1;
   float* mlp_a;
+  // operands of the MFMA projections (layers with max_batch > 1): o, h1 * gamma2
+  // and SiLU(g) * u split into bf16 levels in lane order, and RMSNorm2's
+  // per-stripe sums of squares
+  uint16_t* op_o = nullptr;
+  uint16_t* op_gu = nullptr;
+  uint16_t* op_down = nullptr;
+  float* ssq_h1 = nullptr;
+  int nbtc = 0;        // batch tiles of the operand buffers
+  int gemm_path = FASTTPS_GEMM_AUTO;
   // the op-by-op baseline's scratch (fasttps_unfused_enable)
   void* uf_arena = nullptr;
   UnfusedArgs uf{};
@@ -93,6 +140,12 @@ struct fasttps_weights {
   uint16_t* w_down;
   uint16_t* attn_norm;
   uint16_t* mlp_norm;
+  // MFMA tiles (16 rows x 32 inputs in operand order), packed for layers with
+  // max_batch > 1; null otherwise
+  uint16_t* t_qkv = nullptr;
+  uint16_t* t_o = nullptr;
+  uint16_t* t_gu = nullptr;
+  uint16_t* t_down = nullptr;
 };
 
 namespace {
@@ -202,7 +255,10 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
     }
   }
 
-  size_t sizes[7] = {
+  const bool mfma = B > 1;
+  const int nbtc = 2 * ceil_div(B, 16);
+  const LayerTiles lt = layer_tiles(c);
+  size_t sizes[11] = {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
@@ -210,9 +266,13 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
       (size_t)B * c.n_heads * d * sizeof(float),
       (size_t)B * c.hidden * sizeof(float),
       (size_t)B * c.intermediate * sizeof(float),
+      mfma ? (size_t)lt.o.kt * nbtc * 512 * sizeof(uint16_t) : 0,
+      mfma ? (size_t)lt.gu.kt * nbtc * 512 * sizeof(uint16_t) : 0,
+      mfma ? (size_t)lt.down.kt * nbtc * 512 * sizeof(uint16_t) : 0,
+      mfma ? (size_t)lt.o.ns * B * sizeof(float) : 0,
   };
-  size_t total = 0, offs[7];
-  for (int i = 0; i < 7; ++i) {
+  size_t total = 0, offs[11];
+  for (int i = 0; i < 11; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -245,10 +305,21 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   l->attn_o = reinterpret_cast<float*>(base + offs[4]);
   l->h1 = reinterpret_cast<float*>(base + offs[5]);
   l->mlp_a = reinterpret_cast<float*>(base + offs[6]);
+  if (mfma) {
+    l->op_o = reinterpret_cast<uint16_t*>(base + offs[7]);
+    l->op_gu = reinterpret_cast<uint16_t*>(base + offs[8]);
+    l->op_down = reinterpret_cast<uint16_t*>(base + offs[9]);
+    l->ssq_h1 = reinterpret_cast<float*>(base + offs[10]);
+    l->nbtc = nbtc;
+  }
 
+  // the operand buffers start at zero: their padding (inputs past the
+  // matrix's last column) must stay zero, since the padded weights are zero
+  // and 0 * NaN is not
   if ((e = hipMemcpy(l->rope_cos, cs.data(), sizes[0], hipMemcpyHostToDevice)) != hipSuccess ||
       (e = hipMemcpy(l->rope_sin, sn.data(), sizes[1], hipMemcpyHostToDevice)) != hipSuccess ||
-      (e = hipMemset(l->mlp_a, 0, sizes[6])) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) {
+      (e = hipMemset(base + offs[2], 0, total - offs[2])) != hipSuccess ||
+      (e = hipDeviceSynchronize()) != hipSuccess) {
     (void)hipFree(arena);
     l->magic = kDeadMagic;
     delete l;
@@ -333,8 +404,13 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   const size_t D = c.hidden, K = c.intermediate, d = c.head_dim;
   const size_t q = (size_t)c.n_heads * d, kv = (size_t)c.n_kv_heads * d;
   const size_t n_qkv = (q + 2 * kv) * D, n_o = D * q, n_gu = 2 * K * D, n_d = K * D;
-  size_t offs[6], sizes[6] = {n_qkv * 2, n_o * 2, n_gu * 2, n_d * 2, D * 2, D * 2}, total = 0;
-  for (int i = 0; i < 6; ++i) {
+  const bool tiled = c.max_batch > 1;
+  const LayerTiles lt = layer_tiles(c);
+  size_t offs[10], sizes[10] = {n_qkv * 2, n_o * 2, n_gu * 2, n_d * 2, D * 2, D * 2,
+                                tiled ? lt.qkv.elems() * 2 : 0, tiled ? lt.o.elems() * 2 : 0,
+                                tiled ? lt.gu.elems() * 2 : 0, tiled ? lt.down.elems() * 2 : 0};
+  size_t total = 0;
+  for (int i = 0; i < 10; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -357,6 +433,12 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   pw->w_down = reinterpret_cast<uint16_t*>(base + offs[3]);
   pw->attn_norm = reinterpret_cast<uint16_t*>(base + offs[4]);
   pw->mlp_norm = reinterpret_cast<uint16_t*>(base + offs[5]);
+  if (tiled) {
+    pw->t_qkv = reinterpret_cast<uint16_t*>(base + offs[6]);
+    pw->t_o = reinterpret_cast<uint16_t*>(base + offs[7]);
+    pw->t_gu = reinterpret_cast<uint16_t*>(base + offs[8]);
+    pw->t_down = reinterpret_cast<uint16_t*>(base + offs[9]);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const auto* g = static_cast<const uint16_t*>(w->w_gate);
   const auto* u = static_cast<const uint16_t*>(w->w_up);
@@ -368,6 +450,14 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
       (e = hipMemcpyAsync(pw->mlp_norm, w->mlp_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, kInterlaceTile, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->w_down, w->w_down, n_d * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (tiled && ((e = launch_tile_weights(pw->w_qkv, nullptr, (int)(q + 2 * kv), (int)D, (int)D, lt.qkv.ns,
+                                          lt.qkv.kt, lt.qkv.rh, pw->t_qkv, s)) != hipSuccess ||
+                 (e = launch_tile_weights(pw->w_o, nullptr, (int)D, (int)q, (int)q, lt.o.ns, lt.o.kt, lt.o.rh,
+                                          pw->t_o, s)) != hipSuccess ||
+                 (e = launch_tile_weights(g, u, (int)K, (int)D, (int)D, lt.gu.ns, lt.gu.kt, lt.gu.rh, pw->t_gu, s)) !=
+                     hipSuccess ||
+                 (e = launch_tile_weights(pw->w_down, nullptr, (int)D, (int)K, (int)K, lt.down.ns, lt.down.kt,
+                                          lt.down.rh, pw->t_down, s)) != hipSuccess)) ||
       (e = hipStreamSynchronize(s)) != hipSuccess) {
     (void)hipStreamSynchronize(s);
     (void)hipFree(arena);
@@ -437,6 +527,13 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
              void* k_cache, void* v_cache, void* y, void* stream, int maxp, int kvf, const KvScales* sc) {
   const fasttps_config& c = l->cfg;
   const size_t D = c.hidden, d = c.head_dim;
+  // projections on the matrix cores from kMfmaMinBatch sequences up (or as
+  // fasttps_set_gemm_path says), where the weights carry MFMA tiles
+  const bool have_tiles = w->t_qkv != nullptr && l->op_o != nullptr;
+  const bool mfma = l->gemm_path == FASTTPS_GEMM_MATRIX ||
+                    (l->gemm_path == FASTTPS_GEMM_AUTO && have_tiles && batch >= kMfmaMinBatch);
+  if (mfma && !have_tiles)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
 
   // attention split: about kTargetAttnBlocks blocks, 64-position tiles
   const int maxn = maxp + 1;
@@ -462,16 +559,41 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     }
   }
 
-  GemvArgs qa{};
-  qa.w = w->w_qkv;
-  qa.rows = (c.n_heads + 2 * c.n_kv_heads) * (int)d;
-  qa.din = (int)D;
-  qa.batch = batch;
-  qa.x_bf16 = xb;
-  qa.gamma = w->attn_norm;
-  qa.out = l->qkv;
-  qa.eps = c.rms_eps;
-  if ((e = launch_rmsnorm_qkv(qa, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
+  const LayerTiles lt = layer_tiles(c);
+  auto mfma_args = [&](const TileDims& td, const uint16_t* wt, int rows, int din) {
+    MfmaArgs m{};
+    m.w = wt;
+    m.ns = td.ns;
+    m.kt = td.kt;
+    m.rh = td.rh;
+    m.nt = ceil_div(td.kt, kMfmaWaves);
+    m.rows = rows;
+    m.din = din;
+    m.batch = batch;
+    m.nbtc = l->nbtc;
+    m.a_out_nbtc = l->nbtc;
+    m.eps = c.rms_eps;
+    return m;
+  };
+
+  if (mfma) {
+    MfmaArgs m = mfma_args(lt.qkv, w->t_qkv, (c.n_heads + 2 * c.n_kv_heads) * (int)d, (int)D);
+    m.x_bf16 = xb;
+    m.gamma = w->attn_norm;
+    m.out = l->qkv;
+    if ((e = launch_mfma_qkv(m, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
+  } else {
+    GemvArgs qa{};
+    qa.w = w->w_qkv;
+    qa.rows = (c.n_heads + 2 * c.n_kv_heads) * (int)d;
+    qa.din = (int)D;
+    qa.batch = batch;
+    qa.x_bf16 = xb;
+    qa.gamma = w->attn_norm;
+    qa.out = l->qkv;
+    qa.eps = c.rms_eps;
+    if ((e = launch_rmsnorm_qkv(qa, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
+  }
 
   AttnArgs aa{};
   aa.qkv = l->qkv;
@@ -481,6 +603,8 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   aa.v_cache = static_cast<uint16_t*>(v_cache);
   aa.part = l->attn_part;
   aa.o = l->attn_o;
+  aa.o_operand = mfma ? l->op_o : nullptr;
+  aa.o_nbtc = l->nbtc;
   aa.batch = batch;
   aa.n_heads = c.n_heads;
   aa.n_kv_heads = c.n_kv_heads;
@@ -496,6 +620,31 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   e = kvf == kKvBf16 ? launch_attention(aa, s, ev[1]) : launch_attention_kv8(aa, *sc, s, ev[1]);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
+
+  if (mfma) {
+    MfmaArgs m = mfma_args(lt.o, w->t_o, (int)D, c.n_heads * (int)d);
+    m.x_bf16 = xb;
+    m.gamma = w->mlp_norm;
+    m.a_in = l->op_o;
+    m.out = l->h1;
+    m.a_out = l->op_gu;
+    m.ssq_out = l->ssq_h1;
+    if ((e = launch_mfma_oproj(m, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
+    m = mfma_args(lt.gu, w->t_gu, c.intermediate, (int)D);
+    m.a_in = l->op_gu;
+    m.ssq_in = l->ssq_h1;
+    m.ns_in = lt.o.ns;
+    m.out = l->mlp_a;
+    m.a_out = l->op_down;
+    if ((e = launch_mfma_gate_up(m, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
+    m = mfma_args(lt.down, w->t_down, (int)D, c.intermediate);
+    m.a_in = l->op_down;
+    m.res_f32 = l->h1;
+    m.out_bf16 = static_cast<uint16_t*>(y);
+    if ((e = launch_mfma_down(m, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
+    if (timed) ++l->prof_n;
+    return FASTTPS_OK;
+  }
 
   GemvArgs oa{};
   oa.w = w->w_o;
@@ -675,6 +824,17 @@ int fasttps_decode_step_unfused(fasttps_layer* l, const fasttps_weights* w, cons
   u.eps = c.rms_eps;
   for (int b = 0; b < batch; ++b) u.pos.p[b] = pos[b];
   if ((e = launch_unfused(u, static_cast<hipStream_t>(stream))) != hipSuccess) return hip_fail(e, "unfused launch");
+  return FASTTPS_OK;
+}
+
+int fasttps_set_gemm_path(fasttps_layer* l, int32_t path) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (path != FASTTPS_GEMM_AUTO && path != FASTTPS_GEMM_VECTOR && path != FASTTPS_GEMM_MATRIX)
+    return fail(FASTTPS_ERR_INVALID_ARG, "unknown projection path %d", path);
+  if (path == FASTTPS_GEMM_MATRIX && !l->op_o)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer with max_batch > 1");
+  l->gemm_path = path;
   return FASTTPS_OK;
 }
 

@@ -56,6 +56,39 @@ hipError_t launch_gate_up(const GemvArgs& a, hipStream_t s, KernelEvents ev = {}
 // out = W act (fp32 in and out), rows of `ld` elements (the op-by-op baseline).
 hipError_t launch_gemv_plain(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
+// Batched projections on the matrix cores: out = W act over weights packed
+// in MFMA tiles (16 rows x 32 inputs, 1 KB, in operand order) and
+// activations split into two bf16 levels (see mfma_proj.hip).
+struct MfmaArgs {
+  const uint16_t* w;        // tiled weights [ns][kt][64 lanes][8] bf16
+  int ns, kt, nt;           // stripes, k-tiles (32 inputs), k-tiles per wave (ceil(kt / 16))
+  int rh;                   // rows per stripe, even, <= 16 (gate/up: rh / 2 units)
+  int sch;                  // stripes per LDS chunk of partial sums (set by the launcher)
+  int rows, din, batch;     // real output rows (gate/up: units K), real inputs, sequences
+  int nbtc;                 // batch tiles (8 sequences) of the a_in buffer
+  const uint16_t* x_bf16;   // QKV: token x [batch, din]; O proj: residual x [batch, rows]
+  const uint16_t* gamma;    // QKV: RMSNorm1 gain [din]; O proj: RMSNorm2 gain [rows]
+  const uint16_t* a_in;     // O proj, gate/up, down: the operand [kt][nbtc][64][8] bf16
+  float* out;               // QKV: q|k|v [batch, rows]; O proj: h1; gate/up: a (fp32)
+  uint16_t* a_out;          // O proj, gate/up: the next projection's operand
+  int a_out_nbtc;           // its batch tiles
+  float* ssq_out;           // O proj: per-stripe sums of h1^2 [ns][batch]
+  const float* ssq_in;      // gate/up: those sums [ns_in][batch]
+  int ns_in;
+  const float* res_f32;     // down: residual h1 [batch, rows]
+  uint16_t* out_bf16;       // down: y [batch, rows] bf16
+  float eps;
+};
+hipError_t launch_mfma_qkv(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});
+hipError_t launch_mfma_oproj(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});
+hipError_t launch_mfma_gate_up(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});
+hipError_t launch_mfma_down(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});
+// the MFMA-tiled copy of a row-major [rows, din] matrix with row stride ld,
+// in stripes of rh rows; with `up` set, stripes of rh / 2 rows of src (gate)
+// and the rh / 2 matching rows of up
+hipError_t launch_tile_weights(const uint16_t* src, const uint16_t* up, int rows, int din, int ld, int ns, int kt,
+                               int rh, uint16_t* dst, hipStream_t s);
+
 struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
   const double* rope_cos;  // [N_max, d/2]
@@ -64,6 +97,8 @@ struct AttnArgs {
   void* v_cache;
   float* part;             // [batch, H, nsplit_cap, d + 2] split partials (m, l, o)
   float* o;                // [batch, H d] fp32
+  uint16_t* o_operand;     // if set: o split for the MFMA O projection [kt][o_nbtc][64][8]
+  int o_nbtc;
   int batch, n_heads, n_kv_heads, head_dim, max_seq;
   int split_len, nsplit, nsplit_cap;
   float scale;             // 1/sqrt(d)

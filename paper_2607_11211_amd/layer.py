@@ -27,6 +27,8 @@ ERR_BAD_HANDLE = -7
 
 DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
 
+GEMM_AUTO, GEMM_VECTOR, GEMM_MATRIX = 0, 1, 2
+
 KV_FP8_E4M3 = 1
 KV_INT8 = 2
 KV_FORMATS = {"fp8_e4m3": KV_FP8_E4M3, "int8": KV_INT8}
@@ -34,7 +36,7 @@ KV_FORMATS = {"fp8_e4m3": KV_FP8_E4M3, "int8": KV_INT8}
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
-           "fasttps_decode_step_kv8", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
+           "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 6
 
 
@@ -70,6 +72,7 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_decode_step_kv8.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, i32, vp, vp, fp, fp, vp, vp]
     lib.fasttps_unfused_enable.argtypes = [vp]
     lib.fasttps_set_attention_p_bf16.argtypes = [vp, i32]
+    lib.fasttps_set_gemm_path.argtypes = [vp, i32]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
     lib.fasttps_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
@@ -84,7 +87,7 @@ def _load() -> ctypes.CDLL:
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
                  "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
-                 "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8"):
+                 "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8", "fasttps_set_gemm_path"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -201,6 +204,10 @@ class Layer:
                                                p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
                                                _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step_unfused")
+
+    def set_gemm_path(self, path: int) -> None:
+        """Projection kernels: GEMM_AUTO, GEMM_VECTOR (GEMVs) or GEMM_MATRIX (MFMA; max_batch > 1)."""
+        _check(LIB.fasttps_set_gemm_path(self.handle, int(path)), "fasttps_set_gemm_path")
 
     def set_attention_p_bf16(self, enable: bool) -> None:
         """Accuracy study only: round the softmax weights to bf16 before PV."""

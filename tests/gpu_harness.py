@@ -34,13 +34,17 @@ def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
     return np.abs(key(a_bits) - key(b_bits))
 
 
-def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=False, kv8=None):
+def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=False, kv8=None, gemm_path=None,
+            max_batch=None):
     """One decode step on cuda:0 through the C ABI (the op-by-op baseline when
     unfused; over an 8-bit cache when kv8 = (fmt, k_codes, v_codes, k_scale,
-    v_scale)). Returns host copies."""
+    v_scale); with the projection kernels forced when gemm_path is set).
+    Returns host copies."""
     import torch
     from paper_2607_11211_amd import layer as L
-    lay = layer if layer is not None else L.Layer(cfg)
+    lay = layer if layer is not None else L.Layer(cfg, max_batch=max_batch)
+    if gemm_path is not None:
+        lay.set_gemm_path(gemm_path)
     W = weights
     if W is None:
         wt = {k: L.to_device(v) for k, v in inp.weights.items()}

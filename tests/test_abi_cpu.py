@@ -44,6 +44,11 @@ def test_unfused_entry_points_reject_bad_handles(L):
     assert L.LIB.fasttps_decode_step_unfused(None, None, None, p, 1, None, None, None, None) == L.ERR_BAD_HANDLE
 
 
+def test_gemm_path_hook_rejects_bad_handles(L):
+    for path in (L.GEMM_AUTO, L.GEMM_VECTOR, L.GEMM_MATRIX, 7):
+        assert L.LIB.fasttps_set_gemm_path(None, path) == L.ERR_BAD_HANDLE
+
+
 def test_kv8_entry_point_rejects_bad_format_and_handles(L):
     p = (ctypes.c_int32 * 1)(0)
     sc = (ctypes.c_float * 1)(1.0)

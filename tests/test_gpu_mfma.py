@@ -1,0 +1,140 @@
+"""The projections on the matrix cores (MFMA, batched decode) against the fp64
+oracle, through the C ABI (MI355X).
+
+Both projection paths are forced on the same shapes: the MFMA kernels
+(weights in operand-order tiles, activations split into two bf16 levels,
+fp32 accumulation) must meet the same bars as the vector GEMVs: untouched
+cache bytes bit-exact, appended K/V within one bf16 ulp, y within
+2e-2 * max(1, |ref|), and the fp32 intermediates (q|k|v, o, h1, a) within
+their bounds. Shapes cover one and two batch tiles, a second grid row
+(more than 16 sequences), ragged positions, matrices whose sizes are not
+multiples of the tile (padding of stripes and k-tiles) and the batched and
+long-context workloads.
+"""
+import numpy as np
+import pytest
+
+from gpu_harness import full_check, log, run_gpu
+from oracle import ref
+from paper_2607_11211_amd import configs, inputs
+from paper_2607_11211_amd.configs import LayerConfig
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_11211_amd.layer  # noqa: F401  (fails loudly if the library is missing)
+
+
+SHAPES = [
+    # one sequence through the MFMA path (a layer built for two)
+    LayerConfig(name="m_b1", index=50, batch=1, hidden=512, n_heads=8, n_kv_heads=2, head_dim=64,
+                intermediate=1376, rope_base=10000.0, max_seq=300, pos=(257,)),
+    # six sequences: one batch tile, GQA group 4, positions 0 and tile edges
+    LayerConfig(name="m_gqa64_b6", index=51, batch=6, hidden=512, n_heads=8, n_kv_heads=2, head_dim=64,
+                intermediate=1376, rope_base=10000.0, max_seq=384, pos=(0, 1, 63, 64, 65, 300)),
+    # nine sequences: two batch tiles; d = 96; hidden 776 is not a multiple of 32 or 16 (padding)
+    LayerConfig(name="m_mha96_b9", index=52, batch=9, hidden=776, n_heads=8, n_kv_heads=8, head_dim=96,
+                intermediate=2056, rope_base=10000.0, max_seq=256,
+                pos=(127, 200, 255, 3, 17, 64, 100, 128, 150)),
+    # twenty sequences: a second grid row of blocks (sequences 16..19)
+    LayerConfig(name="m_b20", index=53, batch=20, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=200,
+                pos=tuple(range(0, 200, 10))),
+    # d = 128, GQA 4, long RoPE base, intermediate not a multiple of 8 units per stripe boundary
+    LayerConfig(name="m_gqa128_b4", index=54, batch=4, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
+                intermediate=2824, rope_base=500000.0, max_seq=1100, pos=(5, 511, 1000, 640)),
+]
+
+
+@pytest.mark.parametrize("cfg", SHAPES, ids=lambda c: c.name)
+@pytest.mark.parametrize("path", ["matrix", "vector"])
+def test_paths_match_oracle(cfg, path):
+    from paper_2607_11211_amd import layer as L
+    gp = L.GEMM_MATRIX if path == "matrix" else L.GEMM_VECTOR
+    log(f"start {cfg.name} {path}")
+    inp = inputs.make_layer_inputs(cfg)
+    r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights)
+    gpu = run_gpu(cfg, inp, gemm_path=gp, max_batch=max(2, cfg.batch))
+    full_check(cfg, inp, gpu, r)
+
+
+@pytest.mark.parametrize("name", ["phi3_batch16_ragged", "gqa_longctx", "phi3_kv1k"])
+def test_workloads_matrix_path(name):
+    from paper_2607_11211_amd import layer as L
+    cfg = configs.get(name)
+    log(f"start {name} matrix")
+    inp = inputs.make_layer_inputs(cfg)
+    cfg = cfg.with_pos(inp.pos)
+    r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights)
+    gpu = run_gpu(cfg, inp, gemm_path=L.GEMM_MATRIX, max_batch=max(2, cfg.batch))
+    full_check(cfg, inp, gpu, r)
+
+
+def test_batch_changes_on_one_handle():
+    """Steps of 16, then 3, then 9 sequences on one handle (the operand
+    buffers keep the larger step's rows), each checked against the oracle."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    big = LayerConfig(name="m_mix", index=55, batch=16, hidden=512, n_heads=8, n_kv_heads=4, head_dim=64,
+                      intermediate=1376, rope_base=10000.0, max_seq=160, pos=tuple(range(5, 160, 10)))
+    inp = inputs.make_layer_inputs(big)
+    lay = L.Layer(big)
+    lay.set_gemm_path(L.GEMM_MATRIX)
+    W = lay.pack({k: L.to_device(v) for k, v in inp.weights.items()})
+    Wf = ref.widen_weights(inp.weights)
+    for nb in (16, 3, 9):
+        cfg = LayerConfig(name=f"m_mix{nb}", index=55, batch=nb, hidden=512, n_heads=8, n_kv_heads=4,
+                          head_dim=64, intermediate=1376, rope_base=10000.0, max_seq=160, pos=big.pos[:nb])
+        x_bits = inputs.make_x(cfg, seed=200 + nb)
+        kc_h, vc_h = inp.k_cache[:nb].copy(), inp.v_cache[:nb].copy()
+        step_inp = inputs.LayerInputs(cfg=cfg, x=x_bits, pos=inp.pos[:nb].copy(), weights=inp.weights,
+                                      k_cache=kc_h, v_cache=vc_h)
+        r = ref.decode_layer_cfg(cfg, x_bits, step_inp.pos, kc_h, vc_h, Wf)
+        gpu = run_gpu(cfg, step_inp, layer=lay, weights=W)
+        full_check(cfg, step_inp, gpu, r)
+    # a rerun of the last step gives identical bits
+    x = L.to_device(x_bits)
+    kc, vc = L.to_device(kc_h), L.to_device(vc_h)
+    y = torch.empty_like(x)
+    lay.step(W, x, step_inp.pos, kc, vc, y)
+    torch.cuda.synchronize()
+    assert np.array_equal(L.from_device(y), gpu["y"])
+    W.free()
+    lay.destroy()
+
+
+def test_path_hook_errors():
+    from paper_2607_11211_amd import layer as L
+    cfg = configs.get("tiny")
+    one = L.Layer(cfg)  # max_batch 1: no MFMA tiles or operands
+    with pytest.raises(L.FastTPSError) as e:
+        one.set_gemm_path(L.GEMM_MATRIX)
+    assert e.value.status == L.ERR_INVALID_ARG
+    with pytest.raises(L.FastTPSError) as e:
+        one.set_gemm_path(5)
+    assert e.value.status == L.ERR_INVALID_ARG
+    one.set_gemm_path(L.GEMM_VECTOR)
+    # weights packed for max_batch 1 carry no tiles: a two-sequence layer
+    # forced onto the matrix path refuses them before any launch
+    inp = inputs.make_layer_inputs(cfg)
+    W1 = one.pack({k: L.to_device(v) for k, v in inp.weights.items()})
+    two = L.Layer(cfg, max_batch=2)
+    two.set_gemm_path(L.GEMM_MATRIX)
+    import torch
+    x = L.to_device(inp.x)
+    kc, vc = L.to_device(inp.k_cache), L.to_device(inp.v_cache)
+    y = torch.zeros_like(x)
+    with pytest.raises(L.FastTPSError) as e:
+        two.step(W1, x, inp.pos, kc, vc, y)
+    assert e.value.status == L.ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert not L.from_device(y).any()
+    assert np.array_equal(L.from_device(kc), inp.k_cache)
+    W1.free()
+    one.destroy()
+    two.destroy()
