@@ -52,6 +52,11 @@ constexpr int kTile = 64;         // positions per tile (4 lanes each)
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head); one combine thread each
 
 constexpr int kRows = kThreads / 16;  // 16-lane DPP rows per block (4 positions each)
+// Online softmax with a lazily moved reference (natural-log units): a lane's
+// weights e^(s - m) stay below e^8 ~ 3e3, so l and o stay far from fp32 range
+// limits over any split, and (m, l, o) of different lanes and splits combine
+// exactly as before (any reference m works in the log-sum-exp merge).
+constexpr float kLazyRescale = 8.0f;
 
 typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 typedef float v2f __attribute__((ext_vector_type(2)));
@@ -275,14 +280,21 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, float kscale,
       for (int e = 0; e < SEG; ++e) sc = fmaf(G == 1 ? qr[e] : sm.q[h][seg * SEG + e], kf[e], sc);
       sc = quad_sum(sc) * scale;
       if (valid) {
-        const float mn = fmaxf(m[h], sc);
-        const float cf = merge_factor(m[h], mn);
-        const float p = __expf(sc - mn);
-        l[h] = fmaf(l[h], cf, p);
+        // the reference m moves only when a score passes it by more than
+        // kLazyRescale (then l and o are rescaled once); p = e^(s - m) <=
+        // e^kLazyRescale otherwise, and each position costs one FMA per element
+        if (sc > m[h] + kLazyRescale) {
+          const float cf = merge_factor(m[h], sc);
+          l[h] *= cf;
+#pragma unroll
+          for (int e = 0; e < SEG; ++e) o[h][e] *= cf;
+          m[h] = sc;
+        }
+        const float p = __expf(sc - m[h]);
+        l[h] += p;
         const float pv = PBF16 ? bf16_to_f32(f32_to_bf16(p)) : p;
 #pragma unroll
-        for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(o[h][e], cf, pv * vf[e]);
-        m[h] = mn;
+        for (int e = 0; e < SEG; ++e) o[h][e] = fmaf(pv, vf[e], o[h][e]);
       }
     }
   };

@@ -535,13 +535,21 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   if (mfma && !have_tiles)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
 
-  // attention split: about kTargetAttnBlocks blocks, 64-position tiles
+  // attention split: positions of all (sequence, kv head) pairs dealt in
+  // splits of split_len (tiles of 64) so that about kTargetAttnBlocks blocks
+  // carry the work; ragged batches get twice as many, shorter splits, so the
+  // longest split sets less of the kernel's time
   const int maxn = maxp + 1;
-  const int per_bg = ceil_div(kTargetAttnBlocks, batch * c.n_kv_heads);
-  int nsplit = std::min({per_bg, ceil_div(maxn, kAttnTile), l->nsplit_cap});
-  nsplit = std::max(nsplit, 1);
-  const int split_len = round_up(ceil_div(maxn, nsplit), kAttnTile);
-  nsplit = ceil_div(maxn, split_len);
+  long total = 0;
+  int minp = maxp;
+  for (int b = 0; b < batch; ++b) {
+    total += pos[b] + 1;
+    minp = std::min(minp, (int)pos[b]);
+  }
+  const long target = (minp == maxp ? 1 : 2) * (long)kTargetAttnBlocks;
+  int split_len = round_up((int)std::min<long>((total * c.n_kv_heads + target - 1) / target, maxn), kAttnTile);
+  split_len = std::max(split_len, round_up(ceil_div(maxn, l->nsplit_cap), kAttnTile));
+  const int nsplit = ceil_div(maxn, split_len);
 
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
