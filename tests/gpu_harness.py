@@ -1,5 +1,12 @@
 """Helpers of the GPU parity tests: run the HIP layer through the C ABI and
-compare it with the fp64 oracle on the same seeded inputs."""
+compare it with the fp64 oracle on the same seeded inputs.
+
+The appended K/V are held to one bf16 ulp of the oracle's exact values
+(reading R16); where the GPU's rounding of an entry lands on the other
+neighbour, the attention and everything after it are compared with the
+oracle run on the GPU's stored entries (reading R9: attention reads the
+stored entry), so that one legitimate rounding is not charged to the
+attention's 1e-4 bar."""
 from __future__ import annotations
 
 import sys
@@ -149,8 +156,25 @@ def check_intermediates(cfg, inp, gpu, r):
     return worst
 
 
+def appended_entries(cfg, inp, gpu):
+    """The GPU's appended K and V slots, [B, H_kv, d] bits each."""
+    B = cfg.batch
+    gk = np.stack([gpu["k_cache"][b, :, int(inp.pos[b]), :] for b in range(B)])
+    gv = np.stack([gpu["v_cache"][b, :, int(inp.pos[b]), :] for b in range(B)])
+    return gk, gv
+
+
 def full_check(cfg, inp, gpu, r, intermediates=True):
+    """The cache against the oracle (untouched bytes exact, appended entries
+    within one ulp); y and the intermediates against the oracle run on the
+    GPU's own appended entries where those differ from the oracle's (the
+    attention reads the stored, rounded entry; a one-ulp rounding of it
+    would otherwise be charged to the attention and everything after it)."""
     stats = check_cache(cfg, inp, gpu, r)
+    gk, gv = appended_entries(cfg, inp, gpu)
+    if not (np.array_equal(gk, r["k_new_bits"]) and np.array_equal(gv, r["v_new_bits"])):
+        r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights, new_entries=(gk, gv))
+        stats["teacher_forced"] = True
     yerr = check_y(gpu, r)
     worst = check_intermediates(cfg, inp, gpu, r) if intermediates else {}
     log(f"{cfg.name}: pos={inp.pos.tolist()[:8]} y_err={yerr:.2e} cache={stats} inter={worst}")
