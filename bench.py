@@ -59,6 +59,7 @@ def kernel_bytes(cfg, pos):
         "oproj_residual": 2 * D * cfg.q_dim,
         "mlp_gate_up": 2 * 2 * K * D + 2 * D,
         "mlp_down": 2 * K * D,
+        "fused_layer": cfg.step_bytes(pos),
     }
 
 
@@ -270,8 +271,9 @@ def main() -> int:
                          "one JSON line per point, instead of the benchmark")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip timing the op-by-op baseline (Alg. 1 + Alg. 2 operators, Concat reloading the cache)")
-    ap.add_argument("--gemm", choices=["auto", "vector", "matrix"], default="auto",
-                    help="projection kernels: vector GEMVs, MFMA (matrix cores), or the library's choice by batch")
+    ap.add_argument("--gemm", choices=["auto", "vector", "matrix", "fused"], default="auto",
+                    help="projection kernels: vector GEMVs (six kernels per step), MFMA (matrix cores), the fused "
+                         "one-kernel step (one sequence), or the library's choice")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="finish with a plain 256 MiB device copy (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -299,7 +301,7 @@ def main() -> int:
     nl = cfg.layers if cfg.layers > 1 else max(1, -(-ROTATE_BYTES // cfg.step_bytes(pos)))
     log(f"workload {cfg.name}: {nl} layers, batch {cfg.batch}, pos {pos.tolist()[:4]}")
 
-    gemm = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX}[args.gemm]
+    gemm = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX, "fused": L.GEMM_FUSED}[args.gemm]
     lay = L.Layer(cfg, max_batch=max(cfg.batch, 2) if args.gemm == "matrix" else None)
     lay.set_gemm_path(gemm)
     weights, kcs, vcs = [], [], []
@@ -352,7 +354,8 @@ def main() -> int:
         step()
     kms = lay.profile_end(nprof)
     names = L.kernel_names()
-    kern_us = {n: float(np.mean(kms[:, i]) * 1e3) for i, n in enumerate(names)}
+    # kernels the step launched (the others read 0)
+    kern_us = {n: float(np.mean(kms[:, i]) * 1e3) for i, n in enumerate(names) if np.any(kms[:, i] > 0)}
     log("kernels (us): " + ", ".join(f"{n} {v:.2f}" for n, v in kern_us.items()))
 
     # HIP-graph replay of the whole decode step

@@ -181,6 +181,9 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
  *                        accumulation); needs max_batch > 1, for which
  *                        fasttps_weights_pack also stores the weights in the
  *                        MFMA tile order (about twice the weight memory)
+ *   FASTTPS_GEMM_FUSED   one sequence in one persistent kernel (below); a
+ *                        measured alternative, slower on MI355X than the six
+ *                        kernels of the vector path replayed from a HIP graph
  *   FASTTPS_GEMM_AUTO    (default) the matrix path from 2 sequences up where
  *                        the weights carry the tiles, else the vector path
  * At batch 8-16 the projections are dense enough that the multiply-adds
@@ -193,6 +196,10 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
 #define FASTTPS_GEMM_AUTO 0
 #define FASTTPS_GEMM_VECTOR 1
 #define FASTTPS_GEMM_MATRIX 2
+#define FASTTPS_GEMM_FUSED 3  /* one sequence: the whole step as one persistent kernel
+                                 (the vector GEMVs and the attention as phases of one
+                                 launch); shapes it is built for, else the step fails
+                                 with FASTTPS_ERR_UNSUPPORTED before any launch */
 FASTTPS_API int fasttps_set_gemm_path(fasttps_layer* layer, int32_t path);
 
 /* Accuracy-study hook: when enabled, later steps of this layer handle round
@@ -215,6 +222,9 @@ FASTTPS_API int fasttps_set_attention_p_bf16(fasttps_layer* layer, int32_t enabl
 #define FASTTPS_DBG_ATTN  1
 #define FASTTPS_DBG_H1    2
 #define FASTTPS_DBG_MLP_A 3
+#define FASTTPS_DBG_FUSED_WAITS 4  /* int32 [1]: bounded waits of the fused kernel that ran
+                                      out since the layer was created (0 when every phase
+                                      hand-over completed); `batch` is ignored */
 FASTTPS_API int fasttps_debug_read(fasttps_layer* layer, int32_t which, int32_t batch, void* dst,
                        size_t bytes, void* stream);
 
@@ -226,7 +236,8 @@ FASTTPS_API int fasttps_debug_read(fasttps_layer* layer, int32_t which, int32_t 
  * n_steps recorded steps (at most max_steps), and releases the events.
  * Kernel k is named by fasttps_kernel_name(k). Steps beyond max_steps run
  * untimed. Not for use under stream capture. */
-#define FASTTPS_NUM_KERNELS 6
+#define FASTTPS_NUM_KERNELS 7  /* the six kernels of the separate path, then the fused kernel;
+                                  a kernel a step does not launch reads 0 */
 FASTTPS_API int fasttps_profile_begin(fasttps_layer* layer, int32_t max_steps);
 FASTTPS_API int fasttps_profile_end(fasttps_layer* layer, float* ms, int32_t max_steps, int32_t* n_steps);
 FASTTPS_API const char* fasttps_kernel_name(int32_t k);

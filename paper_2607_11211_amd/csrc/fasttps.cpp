@@ -87,6 +87,10 @@ LayerTiles layer_tiles(const fasttps_config& c) {
   const int rows_qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
   return {pick_tiles(rows_qkv, D, 1), pick_tiles(D, q, 1), pick_tiles(K, D, 2), pick_tiles(D, K, 1)};
 }
+// the fused kernel: phases with a flag per block, and its grid
+constexpr int kFusedPhases = 5;
+constexpr int kFusedBlocks = 256;
+
 // the MFMA path is taken from this batch size up (FASTTPS_GEMM_AUTO)
 constexpr int kMfmaMinBatch = 2;
 constexpr int kMfmaWaves = 16;  // waves per block of the MFMA kernels (they split the k-tiles)
@@ -121,11 +125,17 @@ struct fasttps_layer {
   float* ssq_h1 = nullptr;
   int nbtc = 0;        // batch tiles of the operand buffers
   int gemm_path = FASTTPS_GEMM_AUTO;
+  // the fused kernel's phase hand-over: per-block phase flags, the epoch of
+  // the last completed launch, the count of bounded waits that ran out
+  unsigned* fused_flags = nullptr;
+  unsigned* fused_epoch = nullptr;
+  int* fused_err = nullptr;
   // the op-by-op baseline's scratch (fasttps_unfused_enable)
   void* uf_arena = nullptr;
   UnfusedArgs uf{};
   // per-kernel timing (measurement hook)
   std::vector<hipEvent_t> prof_events;  // [cap][kernel][start, stop]
+  std::vector<uint8_t> prof_used;       // [cap][kernel]: launched with its events
   int prof_cap = 0;
   int prof_n = 0;
 };
@@ -208,6 +218,7 @@ size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 void release_events(fasttps_layer* l) {
   for (hipEvent_t e : l->prof_events) (void)hipEventDestroy(e);
   l->prof_events.clear();
+  l->prof_used.clear();
   l->prof_cap = 0;
   l->prof_n = 0;
 }
@@ -258,7 +269,7 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   const bool mfma = B > 1;
   const int nbtc = 2 * ceil_div(B, 16);
   const LayerTiles lt = layer_tiles(c);
-  size_t sizes[11] = {
+  size_t sizes[12] = {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
@@ -270,9 +281,10 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
       mfma ? (size_t)lt.gu.kt * nbtc * 512 * sizeof(uint16_t) : 0,
       mfma ? (size_t)lt.down.kt * nbtc * 512 * sizeof(uint16_t) : 0,
       mfma ? (size_t)lt.o.ns * B * sizeof(float) : 0,
+      (size_t)kFusedPhases * kFusedBlocks * sizeof(unsigned) + 2 * sizeof(unsigned),
   };
-  size_t total = 0, offs[11];
-  for (int i = 0; i < 11; ++i) {
+  size_t total = 0, offs[12];
+  for (int i = 0; i < 12; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -312,6 +324,9 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
     l->ssq_h1 = reinterpret_cast<float*>(base + offs[10]);
     l->nbtc = nbtc;
   }
+  l->fused_flags = reinterpret_cast<unsigned*>(base + offs[11]);
+  l->fused_epoch = l->fused_flags + kFusedPhases * kFusedBlocks;
+  l->fused_err = reinterpret_cast<int*>(l->fused_epoch + 1);
 
   // the operand buffers start at zero: their padding (inputs past the
   // matrix's last column) must stay zero, since the padded weights are zero
@@ -347,8 +362,8 @@ int fasttps_layer_destroy(fasttps_layer* l) {
 }
 
 const char* fasttps_kernel_name(int32_t k) {
-  static const char* names[FASTTPS_NUM_KERNELS] = {"rmsnorm_qkv", "attention", "attn_combine",
-                                                   "oproj_residual", "mlp_gate_up", "mlp_down"};
+  static const char* names[FASTTPS_NUM_KERNELS] = {"rmsnorm_qkv",    "attention",   "attn_combine", "oproj_residual",
+                                                   "mlp_gate_up", "mlp_down", "fused_layer"};
   return (k >= 0 && k < FASTTPS_NUM_KERNELS) ? names[k] : "";
 }
 
@@ -358,6 +373,7 @@ int fasttps_profile_begin(fasttps_layer* l, int32_t max_steps) {
   if (max_steps < 1 || max_steps > (1 << 16)) return fail(FASTTPS_ERR_INVALID_ARG, "max_steps out of range");
   release_events(l);
   l->prof_events.resize((size_t)max_steps * FASTTPS_NUM_KERNELS * 2, nullptr);
+  l->prof_used.assign((size_t)max_steps * FASTTPS_NUM_KERNELS, 0);
   for (auto& ev : l->prof_events) {
     hipError_t e = hipEventCreate(&ev);
     if (e != hipSuccess) {
@@ -378,11 +394,18 @@ int fasttps_profile_end(fasttps_layer* l, float* ms, int32_t max_steps, int32_t*
   const int n = std::min(l->prof_n, (int)max_steps);
   *n_steps = n;
   hipError_t e = hipSuccess;
-  if (l->prof_n > 0) e = hipEventSynchronize(l->prof_events[((size_t)l->prof_n * FASTTPS_NUM_KERNELS - 1) * 2 + 1]);
+  // the last launched kernel of the last recorded step
+  if (l->prof_n > 0) {
+    const size_t st = (size_t)(l->prof_n - 1) * FASTTPS_NUM_KERNELS;
+    int kl = FASTTPS_NUM_KERNELS - 1;
+    while (kl > 0 && !l->prof_used[st + kl]) --kl;
+    e = hipEventSynchronize(l->prof_events[(st + kl) * 2 + 1]);
+  }
   for (int i = 0; i < n && e == hipSuccess; ++i)
     for (int k = 0; k < FASTTPS_NUM_KERNELS && e == hipSuccess; ++k) {
-      const size_t j = ((size_t)i * FASTTPS_NUM_KERNELS + k) * 2;
-      e = hipEventElapsedTime(&ms[(size_t)i * FASTTPS_NUM_KERNELS + k], l->prof_events[j], l->prof_events[j + 1]);
+      const size_t j = (size_t)i * FASTTPS_NUM_KERNELS + k;
+      ms[j] = 0.f;
+      if (l->prof_used[j]) e = hipEventElapsedTime(&ms[j], l->prof_events[2 * j], l->prof_events[2 * j + 1]);
     }
   release_events(l);
   if (e != hipSuccess) return hip_fail(e, "kernel timing");
@@ -551,6 +574,24 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   split_len = std::max(split_len, round_up(ceil_div(maxn, l->nsplit_cap), kAttnTile));
   const int nsplit = ceil_div(maxn, split_len);
 
+  // one sequence: the whole step as one persistent kernel, on request
+  // (FASTTPS_GEMM_FUSED), where it is built for the shape and the step is the
+  // plain bf16-cache step. Not the automatic choice: on MI355X its phase
+  // hand-overs through coherent flags cost more than the six kernels'
+  // boundaries in a HIP graph (85 vs 62 us per Phi-3 layer at KV 4096).
+  FusedShape fsh{};
+  fsh.head_dim = (int)d;
+  fsh.group = c.n_heads / c.n_kv_heads;
+  fsh.q = gemv_shape_b1((int)D, false);
+  fsh.o = gemv_shape_b1(c.n_heads * (int)d, false);
+  fsh.gu = gemv_shape_b1((int)D, true);
+  fsh.down = gemv_shape_b1(c.intermediate, false);
+  const bool fused_ok = batch == 1 && kvf == kKvBf16 && l->p_bf16 == 0 && nsplit <= 64 &&
+                        ceil_div(c.n_heads * (int)d, kFusedBlocks) * nsplit <= 1024 && fused_layer_supported(fsh);
+  const bool fused = !mfma && l->gemm_path == FASTTPS_GEMM_FUSED;
+  if (fused && !fused_ok)
+    return fail(FASTTPS_ERR_UNSUPPORTED, "the fused kernel is built for one sequence of the Phi-3-mini layer shape");
+
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -566,42 +607,47 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
       ev[k].stop = l->prof_events[i + 1];
     }
   }
-
-  const LayerTiles lt = layer_tiles(c);
-  auto mfma_args = [&](const TileDims& td, const uint16_t* wt, int rows, int din) {
-    MfmaArgs m{};
-    m.w = wt;
-    m.ns = td.ns;
-    m.kt = td.kt;
-    m.rh = td.rh;
-    m.nt = ceil_div(td.kt, kMfmaWaves);
-    m.rows = rows;
-    m.din = din;
-    m.batch = batch;
-    m.nbtc = l->nbtc;
-    m.a_out_nbtc = l->nbtc;
-    m.eps = c.rms_eps;
-    return m;
+  auto used = [&](int k) {
+    if (timed) l->prof_used[(size_t)l->prof_n * FASTTPS_NUM_KERNELS + k] = 1;
   };
 
-  if (mfma) {
-    MfmaArgs m = mfma_args(lt.qkv, w->t_qkv, (c.n_heads + 2 * c.n_kv_heads) * (int)d, (int)D);
-    m.x_bf16 = xb;
-    m.gamma = w->attn_norm;
-    m.out = l->qkv;
-    if ((e = launch_mfma_qkv(m, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
-  } else {
-    GemvArgs qa{};
-    qa.w = w->w_qkv;
-    qa.rows = (c.n_heads + 2 * c.n_kv_heads) * (int)d;
-    qa.din = (int)D;
-    qa.batch = batch;
-    qa.x_bf16 = xb;
-    qa.gamma = w->attn_norm;
-    qa.out = l->qkv;
-    qa.eps = c.rms_eps;
-    if ((e = launch_rmsnorm_qkv(qa, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
-  }
+  // the vector path's arguments (also the fused kernel's phases)
+  GemvArgs qa{};
+  qa.w = w->w_qkv;
+  qa.rows = (c.n_heads + 2 * c.n_kv_heads) * (int)d;
+  qa.din = (int)D;
+  qa.batch = batch;
+  qa.x_bf16 = xb;
+  qa.gamma = w->attn_norm;
+  qa.out = l->qkv;
+  qa.eps = c.rms_eps;
+  GemvArgs oa{};
+  oa.w = w->w_o;
+  oa.rows = (int)D;
+  oa.din = c.n_heads * (int)d;
+  oa.batch = batch;
+  oa.x_bf16 = xb;
+  oa.in_f32 = l->attn_o;
+  oa.out = l->h1;
+  oa.eps = c.rms_eps;
+  GemvArgs ga{};
+  ga.w = w->w_gu;
+  ga.rows = c.intermediate;
+  ga.din = (int)D;
+  ga.batch = batch;
+  ga.gamma = w->mlp_norm;
+  ga.in_f32 = l->h1;
+  ga.out = l->mlp_a;
+  ga.eps = c.rms_eps;
+  GemvArgs da{};
+  da.w = w->w_down;
+  da.rows = (int)D;
+  da.din = c.intermediate;
+  da.batch = batch;
+  da.in_f32 = l->mlp_a;
+  da.res_f32 = l->h1;
+  da.out_bf16 = static_cast<uint16_t*>(y);
+  da.eps = c.rms_eps;
 
   AttnArgs aa{};
   aa.qkv = l->qkv;
@@ -625,9 +671,58 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   aa.p_bf16 = l->p_bf16;
   aa.kv_format = kvf;
   for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
+
+  if (fused) {
+    FusedArgs f{};
+    f.qkv = qa;
+    f.oproj = oa;
+    f.gateup = ga;
+    f.down = da;
+    f.attn = aa;
+    f.flags = l->fused_flags;
+    f.epoch = l->fused_epoch;
+    f.err = l->fused_err;
+    f.attn_items = nsplit * c.n_kv_heads;
+    f.stage_floats = std::max({c.n_heads * (int)d, (int)D, c.intermediate});
+    if ((e = launch_fused_layer(f, fsh, s, ev[6])) != hipSuccess) return hip_fail(e, "fused layer launch");
+    used(6);
+    if (timed) ++l->prof_n;
+    return FASTTPS_OK;
+  }
+
+  const LayerTiles lt = layer_tiles(c);
+  auto mfma_args = [&](const TileDims& td, const uint16_t* wt, int rows, int din) {
+    MfmaArgs m{};
+    m.w = wt;
+    m.ns = td.ns;
+    m.kt = td.kt;
+    m.rh = td.rh;
+    m.nt = ceil_div(td.kt, kMfmaWaves);
+    m.rows = rows;
+    m.din = din;
+    m.batch = batch;
+    m.nbtc = l->nbtc;
+    m.a_out_nbtc = l->nbtc;
+    m.eps = c.rms_eps;
+    return m;
+  };
+
+  if (mfma) {
+    MfmaArgs m = mfma_args(lt.qkv, w->t_qkv, qa.rows, (int)D);
+    m.x_bf16 = xb;
+    m.gamma = w->attn_norm;
+    m.out = l->qkv;
+    if ((e = launch_mfma_qkv(m, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
+  } else {
+    if ((e = launch_rmsnorm_qkv(qa, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
+  }
+  used(0);
+
   e = kvf == kKvBf16 ? launch_attention(aa, s, ev[1]) : launch_attention_kv8(aa, *sc, s, ev[1]);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
+  used(1);
   if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
+  used(2);
 
   if (mfma) {
     MfmaArgs m = mfma_args(lt.o, w->t_o, (int)D, c.n_heads * (int)d);
@@ -650,42 +745,14 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     m.res_f32 = l->h1;
     m.out_bf16 = static_cast<uint16_t*>(y);
     if ((e = launch_mfma_down(m, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
-    if (timed) ++l->prof_n;
-    return FASTTPS_OK;
+  } else {
+    if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
+    if ((e = launch_gate_up(ga, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
+    if ((e = launch_down_residual(da, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
   }
-
-  GemvArgs oa{};
-  oa.w = w->w_o;
-  oa.rows = (int)D;
-  oa.din = c.n_heads * (int)d;
-  oa.batch = batch;
-  oa.x_bf16 = xb;
-  oa.in_f32 = l->attn_o;
-  oa.out = l->h1;
-  oa.eps = c.rms_eps;
-  if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
-
-  GemvArgs ga{};
-  ga.w = w->w_gu;
-  ga.rows = c.intermediate;
-  ga.din = (int)D;
-  ga.batch = batch;
-  ga.gamma = w->mlp_norm;
-  ga.in_f32 = l->h1;
-  ga.out = l->mlp_a;
-  ga.eps = c.rms_eps;
-  if ((e = launch_gate_up(ga, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
-
-  GemvArgs da{};
-  da.w = w->w_down;
-  da.rows = (int)D;
-  da.din = c.intermediate;
-  da.batch = batch;
-  da.in_f32 = l->mlp_a;
-  da.res_f32 = l->h1;
-  da.out_bf16 = static_cast<uint16_t*>(y);
-  da.eps = c.rms_eps;
-  if ((e = launch_down_residual(da, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
+  used(3);
+  used(4);
+  used(5);
   if (timed) ++l->prof_n;
   return FASTTPS_OK;
 }
@@ -740,6 +807,7 @@ int fasttps_debug_read(fasttps_layer* l, int32_t which, int32_t batch, void* dst
     case FASTTPS_DBG_ATTN: src = l->attn_o; n = (size_t)c.n_heads * c.head_dim; break;
     case FASTTPS_DBG_H1: src = l->h1; n = (size_t)c.hidden; break;
     case FASTTPS_DBG_MLP_A: src = l->mlp_a; n = (size_t)c.intermediate; break;
+    case FASTTPS_DBG_FUSED_WAITS: src = l->fused_err; n = 1; batch = 1; break;
     default: return fail(FASTTPS_ERR_INVALID_ARG, "unknown debug buffer %d", which);
   }
   n *= (size_t)batch * sizeof(float);
@@ -838,7 +906,8 @@ int fasttps_decode_step_unfused(fasttps_layer* l, const fasttps_weights* w, cons
 int fasttps_set_gemm_path(fasttps_layer* l, int32_t path) {
   g_last_error.clear();
   if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
-  if (path != FASTTPS_GEMM_AUTO && path != FASTTPS_GEMM_VECTOR && path != FASTTPS_GEMM_MATRIX)
+  if (path != FASTTPS_GEMM_AUTO && path != FASTTPS_GEMM_VECTOR && path != FASTTPS_GEMM_MATRIX &&
+      path != FASTTPS_GEMM_FUSED)
     return fail(FASTTPS_ERR_INVALID_ARG, "unknown projection path %d", path);
   if (path == FASTTPS_GEMM_MATRIX && !l->op_o)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer with max_batch > 1");

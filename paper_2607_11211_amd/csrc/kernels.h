@@ -121,6 +121,33 @@ hipError_t launch_attention_kv8(const AttnArgs& a, const KvScales& sc, hipStream
 // combine the split partials into o
 hipError_t launch_attention_combine(const AttnArgs& a, hipStream_t s, KernelEvents ev = {});
 
+// The whole step of one sequence as one persistent kernel (fused_layer.hip):
+// the four projections' arguments (fp32 outputs and inputs in the layer's
+// scratch), the attention's, and the phase hand-over state.
+struct FusedArgs {
+  GemvArgs qkv, oproj, gateup, down;
+  AttnArgs attn;
+  unsigned* flags;   // [5][256] per-block phase flags (epochs)
+  unsigned* epoch;   // the last completed launch's epoch (device)
+  int* err;          // count of bounded waits that ran out (device)
+  int attn_items;    // nsplit * n_kv_heads
+  int stage_floats;  // max(H d, D, K): the LDS stage of a projection's input
+};
+// The launch shapes of the step's projections (GEMV chunks per lane, segments
+// per half row, rows in flight) and the attention's head dimension and group.
+struct FusedShape {
+  struct Gemv {
+    int maxch, nseg_h, nbuf;
+    bool operator==(const Gemv& o) const { return maxch == o.maxch && nseg_h == o.nseg_h && nbuf == o.nbuf; }
+  };
+  int head_dim, group;
+  Gemv q, o, gu, down;
+};
+bool fused_layer_supported(const FusedShape& sh);
+hipError_t launch_fused_layer(const FusedArgs& f, const FusedShape& sh, hipStream_t s, KernelEvents ev = {});
+// the launch shape the separate GEMV kernels use for one sequence
+FusedShape::Gemv gemv_shape_b1(int din, bool gate_up);
+
 // The op-by-op baseline (Alg. 1 + Alg. 2, every intermediate through HBM).
 struct UnfusedArgs {
   const uint16_t* x;                       // [B, D] bf16

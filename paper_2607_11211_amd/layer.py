@@ -25,9 +25,9 @@ ERR_OOM = -5
 ERR_HIP = -6
 ERR_BAD_HANDLE = -7
 
-DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A = 0, 1, 2, 3
+DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A, DBG_FUSED_WAITS = 0, 1, 2, 3, 4
 
-GEMM_AUTO, GEMM_VECTOR, GEMM_MATRIX = 0, 1, 2
+GEMM_AUTO, GEMM_VECTOR, GEMM_MATRIX, GEMM_FUSED = 0, 1, 2, 3
 
 KV_FP8_E4M3 = 1
 KV_INT8 = 2
@@ -37,7 +37,7 @@ EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step"
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
            "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
-NUM_KERNELS = 6
+NUM_KERNELS = 7
 
 
 class FastTPSError(RuntimeError):
@@ -206,8 +206,18 @@ class Layer:
                "fasttps_decode_step_unfused")
 
     def set_gemm_path(self, path: int) -> None:
-        """Projection kernels: GEMM_AUTO, GEMM_VECTOR (GEMVs) or GEMM_MATRIX (MFMA; max_batch > 1)."""
+        """Projection kernels: GEMM_AUTO, GEMM_VECTOR (GEMVs), GEMM_MATRIX (MFMA; max_batch > 1)
+        or GEMM_FUSED (one sequence, the whole step as one persistent kernel)."""
         _check(LIB.fasttps_set_gemm_path(self.handle, int(path)), "fasttps_set_gemm_path")
+
+    def fused_wait_errors(self) -> int:
+        """Bounded waits of the fused kernel that ran out since the layer was created."""
+        import torch
+        t = torch.zeros(1, dtype=torch.int32, device="cuda")
+        _check(LIB.fasttps_debug_read(self.handle, DBG_FUSED_WAITS, 1, _ptr(t), 4, _stream_handle(None)),
+               "fasttps_debug_read")
+        torch.cuda.synchronize()
+        return int(t.item())
 
     def set_attention_p_bf16(self, enable: bool) -> None:
         """Accuracy study only: round the softmax weights to bf16 before PV."""
