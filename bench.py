@@ -63,20 +63,38 @@ def kernel_bytes(cfg, pos):
     }
 
 
-def source_digest(path: str) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha1(f.read()).hexdigest()
+# the sources each kernel is built from (a digest of them keys the committed
+# counter results to the code they were taken on)
+CSRC = "paper_2607_11211_amd/csrc/"
+KERNEL_SOURCES = {
+    "gemv": [CSRC + "gemv.hip", CSRC + "gemv_body.h", CSRC + "common.h", CSRC + "kernels.h"],
+    # the split count (and so the partial-result traffic) is chosen on the host
+    "attention": [CSRC + "attention.hip", CSRC + "attn_body.h", CSRC + "common.h", CSRC + "kernels.h",
+                  CSRC + "fasttps.cpp"],
+    "mfma": [CSRC + "mfma_proj.hip", CSRC + "common.h", CSRC + "kernels.h"],
+    "fused": [CSRC + "fused_layer.hip", CSRC + "gemv_body.h", CSRC + "attn_body.h", CSRC + "common.h",
+              CSRC + "kernels.h", CSRC + "fasttps.cpp"],
+}
+KERNEL_GROUP = {"rmsnorm_qkv": "gemv", "oproj_residual": "gemv", "mlp_gate_up": "gemv", "mlp_down": "gemv",
+                "attention": "attention", "attn_combine": "attention", "fused_layer": "fused"}
+
+
+def source_digest(paths) -> str:
+    h = hashlib.sha1()
+    for p in ([paths] if isinstance(paths, str) else paths):
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def load_traffic(kernel: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the kernel source as it is now; else None."""
+    taken on the kernel's sources as they are now; else None."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
         info = json.load(open(TRAFFIC_FILE))[kernel]
-        src = os.path.join(ROOT, info["source"])
-        if source_digest(src) != info["source_sha1"]:
+        if source_digest(info["sources"]) != info["sources_sha1"]:
             return None
         return float(info["bytes_per_launch"])
     except Exception:
