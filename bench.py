@@ -156,10 +156,34 @@ def cpu_baseline(cfg, seconds: float):
         if (el >= seconds and reps >= 3) or reps >= 100000:
             break
     us = el / reps * 1e6
+    # the same sample on one core (BLAS limited to one thread), for a shorter time
+    us1, reps1, el1 = None, 0, 0.0
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"):
+            t0 = time.perf_counter()
+            while True:
+                ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, W)
+                reps1 += 1
+                el1 = time.perf_counter() - t0
+                if (el1 >= seconds / 2 and reps1 >= 2) or reps1 >= 100000:
+                    break
+        us1 = el1 / reps1 * 1e6
+    except Exception:
+        us1 = None
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
     return {"value": round(us, 1), "unit": "us", "cores": int(cores), "kind": "oracle",
             "sample": f"one layer ({cfg.name} shape, layer 0 inputs), {reps} repetitions in {el:.1f} s, "
                       f"fp64 numpy, BLAS threads {threads}",
-            "gbps": round(cfg.step_bytes() / us * 1e-3, 2)}
+            "gbps": round(cfg.step_bytes() / us * 1e-3, 2),
+            "value_one_core": round(us1, 1) if us1 is not None else None,
+            "one_core_sample": f"{reps1} repetitions in {el1:.1f} s, BLAS threads 1" if us1 is not None else None,
+            "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
 
 
 def read_ceiling(nbytes: int = 4 << 30):
@@ -297,7 +321,7 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs one decode layer on one GPU; --gpus {args.gpus} is not supported "
-              "(the multi-GPU sharding plan is described in DESIGN.md, not implemented)", file=sys.stderr)
+              "(sharding across GPUs is not implemented)", file=sys.stderr)
         return 2
 
     import torch
