@@ -4,9 +4,14 @@
 // softmax and PV for one head inside one core's L1. One head's work is far
 // too small for a 256-CU chip, so here the softmax-independent axis the paper
 // uses (heads) is combined with a split of the cached positions:
-//   grid = (split, kv head g, sequence b); a block covers positions
-//   [s*L, s*L + L) of one (b, g) for all G = H/H_kv query heads of that KV
-//   head, so each K/V byte is read from HBM once (grouped-query attention).
+//   grid = (split, kv head g, sequence b); of the tiles of 64 positions of
+//   one (b, g), split s of S takes tiles s, s + S, s + 2S, ... for all
+//   G = H/H_kv query heads of that KV head, so each K/V byte is read from HBM
+//   once (grouped-query attention). The splits of a head are interleaved
+//   rather than contiguous ranges so that at any moment the blocks of a head
+//   read one compact window of the cache, as the GEMVs deal their rows
+//   (contiguous ranges left some split lengths of the batched and ragged
+//   workloads several percent slower on MI355X).
 // Per block (256 threads, tiles of 64 positions):
 //   * four lanes share a position, each owning a quarter of d: a lane loads
 //     exactly the K and V chunks it computes with (the four lanes of a
@@ -15,7 +20,8 @@
 //     has no barrier;
 //   * the prologue's few loads go out first, then the ring: a wave's loads
 //     return in the order they were issued. Every load is issued
-//     unconditionally (rows past the split are clamped into it and masked),
+//     unconditionally (rows past the sequence are clamped to its last entry
+//     and masked),
 //     so the compiler waits for exactly the tile it needs;
 //   * prologue: RoPE on the G query heads and on k, with shared cos/sin rows
 //     in double precision (Alg. 3 joint RoPE; Eq. 22); the block that owns the

@@ -179,7 +179,7 @@ struct AttnBody {
   const AttnArgs& a;
   IO io;
   Smem& sm;
-  int tid, s, g, b, P, ntot, start, end, last, j, seg, pj, ph;
+  int tid, s, g, b, P, ntot, start, stride, end, last, j, seg, pj, ph;
   bool own_new, live;
   size_t head_off;
   const Chunk* Kc;
@@ -193,15 +193,17 @@ struct AttnBody {
       : a(a_), io(io_), sm(sm_), tid(tid_), s(s_), g(g_), b(b_), live(live_) {
     P = a.pos.p[b];
     ntot = P + 1;
-    start = s * a.split_len;
-    end = live ? min(start + a.split_len, ntot) : start;
-    last = max(end - 1, start);  // a cache row of this split (start < N_max)
+    // tiles s, s + nsplit, ... of the sequence's entries [0, ntot)
+    start = s * kTile;
+    stride = a.nsplit * kTile;
+    end = live ? ntot : start;
+    last = ntot - 1;  // loads past the end read this row (masked)
     head_off = ((size_t)b * a.n_kv_heads + g) * (size_t)a.max_seq * D * kv_bytes<KVF>();  // bytes
     Kc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.k_cache) + head_off);
     Vc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.v_cache) + head_off);
     j = tid >> 2;
     seg = tid & 3;
-    own_new = live && (start <= P) && (P < end);
+    own_new = live && (P / kTile) % a.nsplit == s;  // the split whose tile holds slot P
     pj = tid % HALF;
     ph = min(tid / HALF, G - 1);
   }
@@ -228,7 +230,7 @@ struct AttnBody {
   // ---- the ring's first NRING tiles ----------------------------------------
   __device__ __forceinline__ void prime() {
 #pragma unroll
-    for (int r = 0; r < NRING; ++r) tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, start + r * kTile, last, j, seg);
+    for (int r = 0; r < NRING; ++r) tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, start + r * stride, last, j, seg);
   }
 
   __device__ __forceinline__ void run(float kscale, float vscale) {
@@ -264,7 +266,7 @@ struct AttnBody {
       for (int e = 0; e < SEG; ++e) qr[e] = sm.q[0][seg * SEG + e];
     }
 
-    // ---- main loop over tiles: the cached entries [start, min(end, P)) ----
+    // ---- main loop over the split's tiles: its cached entries below P -----
     float m[G], l[G], o[G][SEG];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -303,10 +305,10 @@ struct AttnBody {
         }
       }
     };
-    for (int t0 = start; t0 < end; t0 += NRING * kTile) {
+    for (int t0 = start; t0 < end; t0 += NRING * stride) {
 #pragma unroll
       for (int r = 0; r < NRING; ++r) {
-        const int tt = t0 + r * kTile;
+        const int tt = t0 + r * stride;
         float kf[SEG], vf[SEG];
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -317,7 +319,7 @@ struct AttnBody {
         // the barrier keeps the refill after the unpack, so the new tile lands
         // in the registers the old one leaves (no copies, no early waits)
         __builtin_amdgcn_sched_barrier(0);
-        tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, tt + NRING * kTile, last, j, seg);
+        tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, tt + NRING * stride, last, j, seg);
         update(kf, vf, tt + j < cend);
       }
     }

@@ -100,7 +100,7 @@ struct AttnArgs {
   uint16_t* o_operand;     // if set: o split for the MFMA O projection [kt][o_nbtc][64][8]
   int o_nbtc;
   int batch, n_heads, n_kv_heads, head_dim, max_seq;
-  int split_len, nsplit, nsplit_cap;
+  int nsplit, nsplit_cap;     // splits per (sequence, KV head): split s takes tiles s, s + nsplit, ...
   float scale;             // 1/sqrt(d)
   int p_bf16;              // accuracy study: softmax weights rounded to bf16 before PV
   int kv_format;           // kKvBf16, kKvFp8 or kKvInt8
