@@ -227,22 +227,16 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     if (tid < a.din / 8) gam[tid] = gload;
     __syncthreads();
   }
-  // the cached operands, once their loads (older than the ring's) are in
-  if constexpr (CACHED) {
+  // the cached operands, once their loads (older than the ring's) are in;
+  // the QKV operands are built from their x chunks during the first stripe
+  // instead, each just before its first MFMA, where the conversion overlaps
+  // the weight stream (built here, all at once, it held the stream ~4 us)
+  if constexpr (CACHED && MODE != MMode::kQkv) {
     const v4u z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-      for (int bt = 0; bt < NBT; ++bt) {
-        if (MODE == MMode::kQkv) {
-          float s2;
-          acache[tt][bt] = qkv_operand(acache[tt][bt], g_chunk(tbase + tt), tbase + tt, bt, s2);
-          ssp[bt] += s2;
-          __builtin_amdgcn_sched_barrier(0);  // one operand at a time: few live temporaries
-        } else {
-          acache[tt][bt] = tbase + tt < a.kt ? acache[tt][bt] : z;
-        }
-      }
+      for (int bt = 0; bt < NBT; ++bt) acache[tt][bt] = tbase + tt < a.kt ? acache[tt][bt] : z;
   }
   if (MODE == MMode::kGateUp) {
     // the wave's share of RMSNorm2's sums (loads issued first, so this waits
@@ -267,7 +261,14 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
         bf16x8 A[NBT];
         if constexpr (CACHED) {
 #pragma unroll
-          for (int bt = 0; bt < NBT; ++bt) A[bt] = as_bf16x8(acache[tt][bt]);
+          for (int bt = 0; bt < NBT; ++bt) {
+            if (MODE == MMode::kQkv && si == 0) {
+              float s2;
+              acache[tt][bt] = qkv_operand(acache[tt][bt], g_chunk(tbase + tt), tbase + tt, bt, s2);
+              ssp[bt] += s2;
+            }
+            A[bt] = as_bf16x8(acache[tt][bt]);
+          }
         } else {
           const int t = tbase + tt;
           const bool live = tt < nt && t < a.kt;
