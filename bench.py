@@ -316,6 +316,9 @@ def main() -> int:
     ap.add_argument("--gemm", choices=["auto", "vector", "matrix", "fused"], default="auto",
                     help="projection kernels: vector GEMVs (six kernels per step), MFMA (matrix cores), the fused "
                          "one-kernel step (one sequence), or the library's choice")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="run the workload with this many sequences instead of its own batch (each at the "
+                         "workload's KV length, or drawn from a ragged workload's range)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="finish with a plain 256 MiB device copy (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -335,6 +338,14 @@ def main() -> int:
         return sweep(args)
     torch.cuda.set_device(0)
     cfg = configs.get(args.workload)
+    text = WORKLOAD_TEXT.get(cfg.name, cfg.name)
+    if args.batch is not None:
+        if not 1 <= args.batch <= 64:
+            print(f"bench.py: --batch {args.batch} is outside 1..64", file=sys.stderr)
+            return 2
+        cfg = dataclasses.replace(cfg, name=f"{cfg.name}_b{args.batch}", batch=args.batch,
+                                  pos=tuple([cfg.pos[0]] * args.batch))
+        text += f"; run with {args.batch} sequences"
     pos = inputs.make_pos(cfg)
     cfg = cfg.with_pos(pos)
     # a single-layer workload runs as a chain of independent copies (own
@@ -515,7 +526,7 @@ def main() -> int:
         "metric": METRIC, "value": round(us_layer, 3), "unit": "us", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": False,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage": "bf16", "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {WORKLOAD_TEXT.get(cfg.name, cfg.name)}"
+        "config": {"workload": f"{cfg.name}: {text}"
                                + ("" if cfg.layers > 1 else f" ({nl} rotating copies)"),
                    "layers": nl, "global_batch": cfg.batch, "seq_len": int(pos.max()) + 1,
                    "parallelism": "single GPU"},
