@@ -6,8 +6,8 @@ Both projection paths are forced on the same shapes: the MFMA kernels
 fp32 accumulation) must meet the same bars as the vector GEMVs: untouched
 cache bytes bit-exact, appended K/V within one bf16 ulp, y within
 2e-2 * max(1, |ref|), and the fp32 intermediates (q|k|v, o, h1, a) within
-their bounds. Shapes cover one and two batch tiles, a second grid row
-(more than 16 sequences), ragged positions, matrices whose sizes are not
+their bounds. Shapes cover one and two batch tiles, a second and a fourth
+grid row (up to the ABI's 64 sequences), ragged positions, matrices whose sizes are not
 multiples of the tile (padding of stripes and k-tiles) and the batched and
 long-context workloads.
 """
@@ -45,6 +45,10 @@ SHAPES = [
     LayerConfig(name="m_b20", index=53, batch=20, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200,
                 pos=tuple(range(0, 200, 10))),
+    # the largest batch the ABI takes (64): four grid rows of MFMA blocks, 16 of vector batch tiles
+    LayerConfig(name="m_b64", index=56, batch=64, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=160,
+                pos=tuple((37 * i) % 151 for i in range(64))),
     # d = 128, GQA 4, long RoPE base, intermediate not a multiple of 8 units per stripe boundary
     LayerConfig(name="m_gqa128_b4", index=54, batch=4, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
                 intermediate=2824, rope_base=500000.0, max_seq=1100, pos=(5, 511, 1000, 640)),
