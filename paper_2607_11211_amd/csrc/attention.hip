@@ -40,7 +40,8 @@
 // split's output (V); the new entry is rounded onto the 8-bit grid once, in
 // double precision, before it is stored and used.
 // A second small kernel combines the splits of each (b, head) with the
-// log-sum-exp identity. (Cross-block tickets are avoided on purpose: on this
+// log-sum-exp identity (one wave per (b, head) up to 64 splits, a block
+// beyond). (Cross-block tickets are avoided on purpose: on this
 // chip an agent-scope fence per block costs far more than a kernel boundary.)
 #include "attn_body.h"
 
@@ -147,6 +148,67 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
   }
 }
 
+// The same merge by one wave per (head, sequence), for up to 64 splits: lane
+// s reads split s's (m, l); the o values of 32 splits at a time are loaded up
+// front (one round trip for up to 32 splits) and merged with each split's
+// factor read from lane s. No block barrier: on the batch-1 Phi-3 layer this
+// saves ~0.5 us per step against the block version.
+constexpr int kWaveCombineChunk = 32;
+template <int D>
+__global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* __restrict__ part, int nsplit,
+                                                                 int nsplit_cap, int n_heads, float* __restrict__ o,
+                                                                 uint16_t* __restrict__ o_operand, int o_nbtc) {
+  constexpr int EPL = (D + kWave - 1) / kWave;  // o elements per lane
+  const int lane = threadIdx.x;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + 2);
+  const int sl = min(lane, nsplit - 1);
+  const float ms = lane < nsplit ? ph[(size_t)sl * (D + 2)] : -INFINITY;
+  const float ls = lane < nsplit ? ph[(size_t)sl * (D + 2) + 1] : 0.f;
+  float ov[kWaveCombineChunk][EPL];
+  auto load_chunk = [&](int s0) {
+#pragma unroll
+    for (int j = 0; j < kWaveCombineChunk; ++j)
+#pragma unroll
+      for (int i = 0; i < EPL; ++i)
+        ov[j][i] = ph[(size_t)min(s0 + j, nsplit - 1) * (D + 2) + 2 + min(lane + kWave * i, D - 1)];
+  };
+  load_chunk(0);
+  const float M = wave_max(ms);
+  const float f = merge_factor(ms, M);  // zero for lanes past the splits
+  const float L = wave_sum(ls * f);
+  float acc[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += kWaveCombineChunk) {
+    if (s0 > 0) load_chunk(s0);
+#pragma unroll
+    for (int j = 0; j < kWaveCombineChunk; ++j) {
+      const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), s0 + j));
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) acc[i] = fmaf(ov[j][i], fj, acc[i]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane + kWave * i;
+    if (e < D) {
+      const float v = acc[i] / L;
+      o[((size_t)b * n_heads + h) * D + e] = v;
+      if (o_operand) {
+        // the MFMA O projection's operand, as in attn_combine_kernel
+        const int k = h * D + e;
+        const uint16_t hi = f32_to_bf16(v);
+        const uint16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
+        const size_t base = (((size_t)(k >> 5) * o_nbtc + b / 8) * kWave + 2 * (b % 8) + 16 * ((k >> 3) & 3)) * 8 +
+                            (k & 7);
+        o_operand[base] = hi;
+        o_operand[base + 8] = lo;
+      }
+    }
+  }
+}
+
 template <int D, int G, int NRING_OVERRIDE = 0>
 hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   // tiles in flight per lane: a tile is D / 8 registers of K and V; the
@@ -190,6 +252,9 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
 template <int D>
 hipError_t launch_combine_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(a.n_heads, a.batch);
+  if (a.nsplit <= kWave)
+    return ext_launch(attn_combine_wave_kernel<D>, grid, dim3(kWave), 0, s, ev, (const float*)a.part, a.nsplit,
+                      a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
   return ext_launch(attn_combine_kernel<D>, grid, dim3(kCombineThreads), 0, s, ev, (const float*)a.part, a.nsplit,
                     a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
 }

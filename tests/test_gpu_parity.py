@@ -33,6 +33,12 @@ SMALL = [
     # GQA group 4, d=128, long base, uneven MLP tile
     LayerConfig(name="s_gqa128", index=12, batch=3, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
                 intermediate=2824, rope_base=500000.0, max_seq=1100, pos=(5, 511, 1000)),
+    # one KV head, long context: 47 splits (the one-wave combine's second chunk of 32)
+    LayerConfig(name="s_kv1_47split", index=14, batch=1, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=3136, pos=(3000,)),
+    # one KV head, longer context: 126 splits (more than a wave: the block combine)
+    LayerConfig(name="s_kv1_126split", index=15, batch=1, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=8064, pos=(8000,)),
     # group 2, batch 9 (two batch tiles of the projections)
     LayerConfig(name="s_g2_b9", index=13, batch=9, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200, pos=(0, 3, 17, 64, 100, 128, 150, 190, 199)),
