@@ -49,17 +49,19 @@ def log(msg: str) -> None:
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_bytes(cfg, pos):
-    """Algorithmic HBM bytes per launch of each kernel (weights once, K/V read once)."""
+def kernel_bytes(cfg, pos, kv_elem_bytes: int = 2):
+    """Algorithmic HBM bytes per launch of each kernel (weights once, K/V read
+    once; an 8-bit cache reads one byte per element)."""
     D, K, d = cfg.hidden, cfg.intermediate, cfg.head_dim
+    kv = cfg.kv_read_bytes(pos) * kv_elem_bytes // 2
     return {
         "rmsnorm_qkv": 2 * cfg.qkv_rows * D + 2 * D,
-        "attention": cfg.kv_read_bytes(pos),
+        "attention": kv,
         "attn_combine": 0,
         "oproj_residual": 2 * D * cfg.q_dim,
         "mlp_gate_up": 2 * 2 * K * D + 2 * D,
         "mlp_down": 2 * K * D,
-        "fused_layer": cfg.step_bytes(pos),
+        "fused_layer": cfg.weight_bytes() + kv,
     }
 
 
@@ -111,7 +113,28 @@ def device_bits(shape, std, mean, gen):
     return t.to(torch.bfloat16).view(torch.int16)
 
 
-def device_layer(cfg, layer, pos, gen):
+def device_cache8(cfg, pos, which, fmt, gen):
+    """An 8-bit cache of codes drawn on the device (the recipe of inputs.make_cache8:
+    finite codes in [0, pos_b), the format's sentinel elsewhere)."""
+    import torch
+    from paper_2607_11211_amd import inputs
+    sentinel = (inputs.K8_SENTINEL if which == "k" else inputs.V8_SENTINEL)[fmt]
+    c = torch.full((cfg.batch, cfg.n_kv_heads, cfg.max_seq, cfg.head_dim), sentinel, dtype=torch.uint8, device="cuda")
+    for b in range(cfg.batch):
+        p = int(pos[b])
+        if p <= 0:
+            continue
+        shape = (cfg.n_kv_heads, p, cfg.head_dim)
+        if fmt == "fp8_e4m3":
+            r = torch.randint(0, 254, shape, generator=gen, device="cuda", dtype=torch.int16)
+            r = torch.where(r < 0x7F, r, r + 1)  # skip the NaN codes 0x7F and 0xFF
+        else:
+            r = torch.randint(-127, 128, shape, generator=gen, device="cuda", dtype=torch.int16) & 0xFF
+        c[b, :, :p].copy_(r.to(torch.uint8))
+    return c
+
+
+def device_layer(cfg, layer, pos, gen, caches=True):
     """Weights and caches of one layer drawn on the device (same recipe as inputs.py)."""
     import torch
     from paper_2607_11211_amd import inputs
@@ -123,6 +146,8 @@ def device_layer(cfg, layer, pos, gen):
         "w_gate": device_bits((K, D), 0.02, 0.0, gen), "w_up": device_bits((K, D), 0.02, 0.0, gen),
         "w_down": device_bits((D, K), 0.02, 0.0, gen),
     }
+    if not caches:
+        return w, None, None
     caches = []
     for sentinel in (inputs.K_SENTINEL, inputs.V_SENTINEL):
         c = torch.full((cfg.batch, cfg.n_kv_heads, cfg.max_seq, cfg.head_dim),
@@ -134,8 +159,9 @@ def device_layer(cfg, layer, pos, gen):
     return w, caches[0], caches[1]
 
 
-def cpu_baseline(cfg, seconds: float):
-    """The fp64 oracle on a bounded sample: layer 0 of the workload, repeated."""
+def cpu_baseline(cfg, seconds: float, kv_fmt: str = "bf16"):
+    """The fp64 oracle on a bounded sample: layer 0 of the workload, repeated
+    (over the same 8-bit cache as the GPU when kv_fmt names one)."""
     from oracle import ref
     from paper_2607_11211_amd import inputs
     try:
@@ -147,10 +173,18 @@ def cpu_baseline(cfg, seconds: float):
     cores = min(threads, len(os.sched_getaffinity(0)))
     inp = inputs.make_layer_inputs(cfg, layer=0)
     W = ref.widen_weights(inp.weights)   # outside the timer
-    ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, W)  # warm
+    kc, vc, kw = inp.k_cache, inp.v_cache, {}
+    if kv_fmt != "bf16":
+        from oracle import kvquant as kq
+        kc = inputs.make_cache8(cfg, inp.pos, "k", kv_fmt)
+        vc = inputs.make_cache8(cfg, inp.pos, "v", kv_fmt)
+        ks = inputs.make_kv_scales(cfg, "k", kv_fmt)
+        vs = inputs.make_kv_scales(cfg, "v", kv_fmt)
+        kw = {"kv": kq.KvQuant(kv_fmt, tuple(float(v) for v in ks), tuple(float(v) for v in vs))}
+    ref.decode_layer_cfg(cfg, inp.x, inp.pos, kc, vc, W, **kw)  # warm
     reps, t0 = 0, time.perf_counter()
     while True:
-        ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, W)
+        ref.decode_layer_cfg(cfg, inp.x, inp.pos, kc, vc, W, **kw)
         reps += 1
         el = time.perf_counter() - t0
         if (el >= seconds and reps >= 3) or reps >= 100000:
@@ -163,7 +197,7 @@ def cpu_baseline(cfg, seconds: float):
         with threadpool_limits(limits=1, user_api="blas"):
             t0 = time.perf_counter()
             while True:
-                ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, W)
+                ref.decode_layer_cfg(cfg, inp.x, inp.pos, kc, vc, W, **kw)
                 reps1 += 1
                 el1 = time.perf_counter() - t0
                 if (el1 >= seconds / 2 and reps1 >= 2) or reps1 >= 100000:
@@ -178,9 +212,10 @@ def cpu_baseline(cfg, seconds: float):
     except OSError:
         pass
     return {"value": round(us, 1), "unit": "us", "cores": int(cores), "kind": "oracle",
-            "sample": f"one layer ({cfg.name} shape, layer 0 inputs), {reps} repetitions in {el:.1f} s, "
-                      f"fp64 numpy, BLAS threads {threads}",
-            "gbps": round(cfg.step_bytes() / us * 1e-3, 2),
+            "sample": f"one layer ({cfg.name} shape, layer 0 inputs"
+                      + (f", {kv_fmt} KV cache" if kv_fmt != "bf16" else "")
+                      + f"), {reps} repetitions in {el:.1f} s, fp64 numpy, BLAS threads {threads}",
+            "gbps": round(kernel_bytes(cfg, cfg.pos, 1 if kv_fmt != "bf16" else 2)["fused_layer"] / us * 1e-3, 2),
             "value_one_core": round(us1, 1) if us1 is not None else None,
             "one_core_sample": f"{reps1} repetitions in {el1:.1f} s, BLAS threads 1" if us1 is not None else None,
             "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
@@ -319,6 +354,9 @@ def main() -> int:
     ap.add_argument("--batch", type=int, default=None,
                     help="run the workload with this many sequences instead of its own batch (each at the "
                          "workload's KV length, or drawn from a ragged workload's range)")
+    ap.add_argument("--kv", choices=["bf16", "fp8_e4m3", "int8"], default="bf16",
+                    help="KV cache element format: bf16, or 8-bit codes with one scale per KV head "
+                         "(fasttps_decode_step_kv8)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="finish with a plain 256 MiB device copy (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -348,25 +386,43 @@ def main() -> int:
         text += f"; run with {args.batch} sequences"
     pos = inputs.make_pos(cfg)
     cfg = cfg.with_pos(pos)
+    kv8 = args.kv != "bf16"
+    if kv8:
+        if args.gemm == "fused":
+            print("bench.py: the one-kernel step reads a bf16 cache only", file=sys.stderr)
+            return 2
+        text += f"; 8-bit KV cache ({args.kv} codes, one scale per KV head)"
+    kb = kernel_bytes(cfg, pos, 1 if kv8 else 2)
+    step_bytes = kb["fused_layer"]
     # a single-layer workload runs as a chain of independent copies (own
     # weights and caches) totalling at least 2 GB, so that no copy is still
     # in the 256 MB Infinity Cache when the chain comes back to it
-    nl = cfg.layers if cfg.layers > 1 else max(1, -(-ROTATE_BYTES // cfg.step_bytes(pos)))
+    nl = cfg.layers if cfg.layers > 1 else max(1, -(-ROTATE_BYTES // step_bytes))
     log(f"workload {cfg.name}: {nl} layers, batch {cfg.batch}, pos {pos.tolist()[:4]}")
 
     gemm = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX, "fused": L.GEMM_FUSED}[args.gemm]
     lay = L.Layer(cfg, max_batch=max(cfg.batch, 2) if args.gemm == "matrix" else None)
     lay.set_gemm_path(gemm)
-    weights, kcs, vcs = [], [], []
+    weights, kcs, vcs, kss, vss = [], [], [], [], []
     gen = torch.Generator(device="cuda")
     gen.manual_seed(0xFA57 + cfg.index)
     host0 = inputs.make_layer_inputs(cfg, layer=0, pos=pos)
     for li in range(nl):
         if li == 0:
             w = {k: L.to_device(v) for k, v in host0.weights.items()}
-            kc, vc = L.to_device(host0.k_cache), L.to_device(host0.v_cache)
+            if kv8:
+                kc = torch.from_numpy(inputs.make_cache8(cfg, pos, "k", args.kv)).cuda()
+                vc = torch.from_numpy(inputs.make_cache8(cfg, pos, "v", args.kv)).cuda()
+            else:
+                kc, vc = L.to_device(host0.k_cache), L.to_device(host0.v_cache)
         else:
-            w, kc, vc = device_layer(cfg, li, pos, gen)
+            w, kc, vc = device_layer(cfg, li, pos, gen, caches=not kv8)
+            if kv8:
+                kc = device_cache8(cfg, pos, "k", args.kv, gen)
+                vc = device_cache8(cfg, pos, "v", args.kv, gen)
+        if kv8:
+            kss.append(inputs.make_kv_scales(cfg, "k", args.kv, layer=li))
+            vss.append(inputs.make_kv_scales(cfg, "v", args.kv, layer=li))
         weights.append(lay.pack(w))
         del w
         kcs.append(kc)
@@ -378,10 +434,16 @@ def main() -> int:
 
     stream = torch.cuda.current_stream()
 
+    def layer_step(li, x, s_):
+        if kv8:
+            lay.step_kv8(weights[li], args.kv, x, pos, kcs[li], vcs[li], kss[li], vss[li], ys[li], s_)
+        else:
+            lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], s_)
+
     def step():
         x = x0
         for li in range(nl):
-            lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], stream)
+            layer_step(li, x, stream)
             x = ys[li]
 
     for _ in range(args.warmup):
@@ -423,7 +485,7 @@ def main() -> int:
                 with torch.cuda.graph(g, stream=s):
                     x = x0
                     for li in range(nl):
-                        lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], s)
+                        layer_step(li, x, s)
                         x = ys[li]
             stream.wait_stream(s)
             torch.cuda.synchronize()
@@ -462,7 +524,9 @@ def main() -> int:
 
     # the op-by-op baseline on the same workload, replayed as a HIP graph
     unfused = None
-    if not args.no_unfused:
+    if kv8 and not args.no_unfused:
+        log("op-by-op baseline: not built for an 8-bit cache; skipped")
+    if not args.no_unfused and not kv8:
         lay.enable_unfused()
         yu = [torch.empty_like(x0) for _ in range(nl)]
 
@@ -499,10 +563,8 @@ def main() -> int:
 
     ms_step = min(stream_ms, graph_ms) if graph_ms is not None else stream_ms
     us_layer = ms_step * 1e3 / nl
-    step_bytes = cfg.step_bytes(pos)
     gbps = step_bytes / (us_layer * 1e-6) / 1e9
 
-    kb = kernel_bytes(cfg, pos)
     dominant = max(kern_us, key=kern_us.get)
     ach = kb[dominant] / (kern_us[dominant] * 1e-6) / 1e9 if kb[dominant] else None
     traffic = load_traffic(dominant)
@@ -519,18 +581,19 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("cpu baseline: timing the fp64 oracle on one layer")
         one = dataclasses.replace(cfg, layers=1)
-        cpu = cpu_baseline(one, args.cpu_seconds)
+        cpu = cpu_baseline(one, args.cpu_seconds, args.kv)
         log(f"cpu baseline: {cpu['value']} us/layer on {cpu['cores']} threads")
 
     out = {
         "metric": METRIC, "value": round(us_layer, 3), "unit": "us", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": False,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage": "bf16", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage": "bf16" if not kv8 else f"bf16 weights, {args.kv} KV cache",
+        "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {text}"
                                + ("" if cfg.layers > 1 else f" ({nl} rotating copies)"),
                    "layers": nl, "global_batch": cfg.batch, "seq_len": int(pos.max()) + 1,
                    "parallelism": "single GPU"},
-        "gemm_path": args.gemm,
+        "gemm_path": args.gemm, "kv_cache": args.kv,
         "hbm_gbps": round(gbps, 1), "hbm_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "read_ceiling": {"gbps": round(ceiling, 1),
                          "method": f"libfasttps_probe stream read of 4 GiB with 16-byte loads, best launch "

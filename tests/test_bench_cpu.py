@@ -78,3 +78,18 @@ def test_several_gpus_are_refused(monkeypatch, capsys):
     monkeypatch.setattr(sys, "argv", ["bench.py", "--gpus", "2"])
     assert bench.main() == 2
     assert "--gpus 2" in capsys.readouterr().err
+
+
+def test_kernel_bytes_of_an_8bit_cache():
+    cfg = configs.get("phi3_kv4k")
+    kb2, kb1 = bench.kernel_bytes(cfg, cfg.pos), bench.kernel_bytes(cfg, cfg.pos, 1)
+    assert kb1["attention"] * 2 == kb2["attention"] == cfg.kv_read_bytes()
+    assert kb1["fused_layer"] == cfg.weight_bytes() + cfg.kv_read_bytes() // 2
+    assert kb1["mlp_gate_up"] == kb2["mlp_gate_up"]
+
+
+@pytest.mark.parametrize("fmt", ["fp8_e4m3", "int8"])
+def test_cpu_baseline_over_an_8bit_cache(fmt):
+    r = bench.cpu_baseline(configs.get("tiny"), 0.2, fmt)
+    assert r["kind"] == "oracle" and r["value"] > 0
+    assert fmt in r["sample"]
