@@ -45,6 +45,10 @@ SHAPES = [
     LayerConfig(name="m_b20", index=53, batch=20, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200,
                 pos=tuple(range(0, 200, 10))),
+    # hidden 8 against the widest MLP the ABI takes (32768): the down projection's k-tiles padded
+    # from 8 inputs and its 32768 inputs in 16 segments (vector) or 1024 k-tiles (MFMA)
+    LayerConfig(name="m_longk", index=57, batch=2, hidden=8, n_heads=1, n_kv_heads=1, head_dim=128,
+                intermediate=32768, rope_base=10000.0, max_seq=70, pos=(69, 3)),
     # the largest batch the ABI takes (64): four grid rows of MFMA blocks, 16 of vector batch tiles
     LayerConfig(name="m_b64", index=56, batch=64, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=160,

@@ -39,6 +39,12 @@ SMALL = [
     # one KV head, longer context: 126 splits (more than a wave: the block combine)
     LayerConfig(name="s_kv1_126split", index=15, batch=1, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=8064, pos=(8000,)),
+    # the smallest shapes the ABI takes: hidden 8 (one 16-byte chunk per row), MLP width 8, a
+    # one-slot cache (position 0: the step attends only its own new entry)
+    LayerConfig(name="s_min", index=16, batch=1, hidden=8, n_heads=1, n_kv_heads=1, head_dim=64,
+                intermediate=8, rope_base=10000.0, max_seq=1, pos=(0,)),
+    LayerConfig(name="s_min_b3", index=17, batch=3, hidden=8, n_heads=2, n_kv_heads=1, head_dim=64,
+                intermediate=8, rope_base=10000.0, max_seq=2, pos=(0, 1, 1)),
     # group 2, batch 9 (two batch tiles of the projections)
     LayerConfig(name="s_g2_b9", index=13, batch=9, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200, pos=(0, 3, 17, 64, 100, 128, 150, 190, 199)),
