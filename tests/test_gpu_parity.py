@@ -71,6 +71,21 @@ def test_workloads(name):
     full_check(cfg, inp, gpu, r)
 
 
+def test_maximum_shape():
+    """The largest shape the ABI takes: hidden 8192, 64 query heads x 128 (GQA group 4), MLP width
+    32768, two sequences; both projection paths against one oracle run."""
+    from paper_2607_11211_amd import layer as L
+    cfg = LayerConfig(name="s_max", index=19, batch=2, hidden=8192, n_heads=64, n_kv_heads=16, head_dim=128,
+                      intermediate=32768, rope_base=500000.0, max_seq=130, pos=(129, 40))
+    log(f"start {cfg.name}: drawing inputs and running the oracle")
+    inp = inputs.make_layer_inputs(cfg)
+    r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights)
+    for path, name in ((L.GEMM_MATRIX, "matrix"), (L.GEMM_VECTOR, "vector")):
+        log(f"{cfg.name}: {name} path")
+        gpu = run_gpu(cfg, inp, gemm_path=path, max_batch=2)
+        full_check(cfg, inp, gpu, r)
+
+
 def test_consecutive_steps_and_determinism():
     """Three tokens in a row on one cache (N_p grows by one per step), and a
     rerun of the same step gives identical bits."""
