@@ -45,6 +45,9 @@ SMALL = [
                 intermediate=8, rope_base=10000.0, max_seq=1, pos=(0,)),
     LayerConfig(name="s_min_b3", index=17, batch=3, hidden=8, n_heads=2, n_kv_heads=1, head_dim=64,
                 intermediate=8, rope_base=10000.0, max_seq=2, pos=(0, 1, 1)),
+    # a 128K-entry context on one KV head: 228 splits (the block combine's loop past its registers)
+    LayerConfig(name="s_ctx128k", index=20, batch=1, hidden=256, n_heads=1, n_kv_heads=1, head_dim=64,
+                intermediate=688, rope_base=500000.0, max_seq=131136, pos=(131072,)),
     # group 2, batch 9 (two batch tiles of the projections)
     LayerConfig(name="s_g2_b9", index=13, batch=9, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200, pos=(0, 3, 17, 64, 100, 128, 150, 190, 199)),
