@@ -462,12 +462,15 @@ def main() -> int:
     stream_ms = e0.elapsed_time(e1) / args.steps
     log(f"stream: {stream_ms:.3f} ms/step, {stream_ms * 1e3 / nl:.2f} us/layer")
 
-    # per-kernel durations (events stamped from each kernel's dispatch)
-    nprof = min(args.steps, 20) * nl
+    # per-kernel durations over K more steps on the same stream, each kernel
+    # bracketed by HIP events stamped at its own dispatch (the stamping costs
+    # host time per launch, so it stays out of the timed steps above)
+    nprof = min(args.steps * nl, 1 << 16)
     lay.profile_begin(nprof)
-    for _ in range(min(args.steps, 20)):
+    for _ in range(args.steps):
         step()
     kms = lay.profile_end(nprof)
+    log(f"per-kernel events over {kms.shape[0]} layer steps")
     names = L.kernel_names()
     # kernels the step launched (the others read 0)
     kern_us = {n: float(np.mean(kms[:, i]) * 1e3) for i, n in enumerate(names) if np.any(kms[:, i] > 0)}
