@@ -4,7 +4,9 @@
 // softmax and PV for one head inside one core's L1. One head's work is far
 // too small for a 256-CU chip, so here the softmax-independent axis the paper
 // uses (heads) is combined with a split of the cached positions:
-//   grid = (split, kv head g, sequence b); of the tiles of 64 positions of
+//   grid = (split, kv head g, sequence b), the sequences in order of
+//   decreasing length (the blocks go out in grid order, so the shortest
+//   blocks fill the end of the kernel); of the tiles of 64 positions of
 //   one (b, g), split s of S takes tiles s, s + S, s + 2S, ... for all
 //   G = H/H_kv query heads of that KV head, so each K/V byte is read from HBM
 //   once (grouped-query attention). The splits of a head are interleaved
@@ -59,7 +61,7 @@ template <int D, int G, int NRING, bool PBF16, int KVF>
 __device__ __forceinline__ void attn_split_body(const AttnArgs& a, float kscale, float vscale) {
   __shared__ attn::AttnSmem<D, G, KVF> sm;
   attn::AttnBody<D, G, NRING, PBF16, KVF, attn::GlobalIO> body(a, attn::GlobalIO{}, sm, threadIdx.x, blockIdx.x,
-                                                               blockIdx.y, blockIdx.z, true);
+                                                               blockIdx.y, a.order.p[blockIdx.z], true);
   body.load_prologue();
   __builtin_amdgcn_sched_barrier(0);  // keep the prologue loads ahead of the tiles
   body.prime();

@@ -678,6 +678,9 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   aa.p_bf16 = l->p_bf16;
   aa.kv_format = kvf;
   for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
+  // the longest sequences' blocks first (ties in batch order)
+  for (int b = 0; b < batch; ++b) aa.order.p[b] = b;
+  std::stable_sort(aa.order.p, aa.order.p + batch, [&](int32_t u, int32_t v) { return pos[u] > pos[v]; });
 
   if (fused) {
     FusedArgs f{};

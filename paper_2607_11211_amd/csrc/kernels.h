@@ -105,6 +105,7 @@ struct AttnArgs {
   int p_bf16;              // accuracy study: softmax weights rounded to bf16 before PV
   int kv_format;           // kKvBf16, kKvFp8 or kKvInt8
   PosArray pos;
+  PosArray order;          // grid z -> sequence: the longest first, so the shortest blocks go last
 };
 // cache element formats (the values of the ABI's FASTTPS_KV_* constants)
 constexpr int kKvBf16 = 0, kKvFp8 = 1, kKvInt8 = 2;
