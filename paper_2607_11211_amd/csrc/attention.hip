@@ -73,10 +73,11 @@ __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
   attn_split_body<D, G, NRING, PBF16, kKvBf16>(a, 1.f, 1.f);
 }
 
-// 8-bit cache: the KV head's two scales come from the argument block
+// 8-bit cache: the KV head's two scales come from the argument block; tiles
+// in flight as for a bf16 cache
 template <int D, int G, int KVF>
 __global__ __launch_bounds__(kThreads) void attn_split_kv8_kernel(AttnArgs a, KvScales sc) {
-  attn_split_body<D, G, 1, false, KVF>(a, sc.k[blockIdx.y], sc.v[blockIdx.y]);
+  attn_split_body<D, G, (G <= 2 ? 2 : 1), false, KVF>(a, sc.k[blockIdx.y], sc.v[blockIdx.y]);
 }
 
 // o[b, h] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s,  M = max_s m_s.
@@ -211,11 +212,13 @@ __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* _
   }
 }
 
-template <int D, int G, int NRING_OVERRIDE = 0>
+template <int D, int G>
 hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   // tiles in flight per lane: a tile is D / 8 registers of K and V; the
-  // query quarter and the softmax state take (D / 4 + 2) G more
-  constexpr int NRING = NRING_OVERRIDE > 0 ? NRING_OVERRIDE : 1;
+  // query quarter and the softmax state take (D / 4 + 2) G more. Two for one
+  // or two query heads (103-226 VGPRs at d = 64-128: at least the two blocks
+  // per CU the split targets), one for groups of four (up to 256 VGPRs)
+  constexpr int NRING = G <= 2 ? 2 : 1;
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
   if (a.p_bf16) return ext_launch(attn_split_kernel<D, G, NRING, true>, grid, dim3(kThreads), 0, s, ev, a);
   return ext_launch(attn_split_kernel<D, G, NRING, false>, grid, dim3(kThreads), 0, s, ev, a);

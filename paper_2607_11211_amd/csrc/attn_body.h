@@ -179,7 +179,7 @@ struct AttnBody {
   const AttnArgs& a;
   IO io;
   Smem& sm;
-  int tid, s, g, b, P, ntot, start, stride, end, last, j, seg, pj, ph;
+  int tid, s, g, b, P, start, stride, end, last, j, seg, pj, ph;
   bool own_new, live;
   size_t head_off;
   const Chunk* Kc;
@@ -192,12 +192,12 @@ struct AttnBody {
                                       bool live_)
       : a(a_), io(io_), sm(sm_), tid(tid_), s(s_), g(g_), b(b_), live(live_) {
     P = a.pos.p[b];
-    ntot = P + 1;
-    // tiles s, s + nsplit, ... of the sequence's entries [0, ntot)
+    // tiles s, s + nsplit, ... of the sequence's cached entries [0, P); the
+    // new entry P is added from LDS by the split whose tile index holds it
     start = s * kTile;
     stride = a.nsplit * kTile;
-    end = live ? ntot : start;
-    last = ntot - 1;  // loads past the end read this row (masked)
+    end = live ? P : start;
+    last = P;  // loads past the end read this row (masked)
     head_off = ((size_t)b * a.n_kv_heads + g) * (size_t)a.max_seq * D * kv_bytes<KVF>();  // bytes
     Kc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.k_cache) + head_off);
     Vc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.v_cache) + head_off);
@@ -277,7 +277,6 @@ struct AttnBody {
     }
     // an 8-bit cache's K scale folds into the softmax scale
     const float scale = KVF == kKvBf16 ? a.scale : a.scale * kscale;
-    const int cend = min(end, P);  // slot P holds the new entry, handled below
     // one step of the online softmax with key kf and value vf
     auto update = [&](const float (&kf)[SEG], const float (&vf)[SEG], bool valid) {
 #pragma unroll
@@ -320,7 +319,7 @@ struct AttnBody {
         // in the registers the old one leaves (no copies, no early waits)
         __builtin_amdgcn_sched_barrier(0);
         tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, tt + NRING * stride, last, j, seg);
-        update(kf, vf, tt + j < cend);
+        update(kf, vf, tt + j < end);
       }
     }
     // the new entry N_p (Eq. 1 slot) from the rounded values in LDS, by the

@@ -23,12 +23,15 @@ namespace {
 constexpr uint64_t kLayerMagic = 0x4641535454505331ull;    // "FASTTPS1"
 constexpr uint64_t kWeightsMagic = 0x4641535454505357ull;  // "FASTTPSW"
 constexpr uint64_t kDeadMagic = 0xDEADDEADDEADDEADull;
-// attention blocks per step (256 CUs): ~3 per CU for one or two query heads
-// per KV head; one per CU for groups of four (twice the registers per
-// block); four times as many, shorter splits when the batch's positions are
-// ragged (measured on MI355X: Phi-3 16-sequence ragged batch 101 -> 94 us,
-// GQA 4 x 32768 115 -> 103 us against 768 blocks throughout)
-constexpr int kTargetAttnBlocks = 768;
+// attention blocks per step (256 CUs): 2 per CU for one or two query heads
+// per KV head (each lane with two tiles in flight); one per CU for groups of
+// four (twice the registers per block); four times as many, shorter splits
+// when the batch's positions are ragged. Measured on MI355X: Phi-3 16-sequence
+// ragged batch 101 -> 94 us and GQA 4 x 32768 115 -> 103 us against 768
+// blocks throughout; then 512 blocks with two tiles in flight against 768
+// with one: Phi-3 layer at KV 4096 61.7 -> 61.2 us per step, 16-sequence
+// ragged batch attention 87.9 -> 86.3 us.
+constexpr int kTargetAttnBlocks = 512;
 constexpr int kTargetAttnBlocksG4 = 256;
 constexpr int kRaggedAttnFactor = 4;
 constexpr int kAttnTile = 64;
@@ -566,14 +569,15 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   if (mfma && !have_tiles)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
 
-  // attention split: the tiles of 64 positions of every (sequence, kv head)
-  // are dealt to nsplit interleaved splits of about split_len positions, so
-  // that about `target` blocks carry the work
-  const int maxn = maxp + 1;
+  // attention split: the tiles of 64 cached positions [0, pos) of every
+  // (sequence, kv head) are dealt to nsplit interleaved splits of about
+  // split_len positions, so that about `target` blocks carry the work (the
+  // new entry at pos comes from registers, so it adds no tile of its own)
+  const int maxn = std::max(maxp, 1);
   long total = 0;
   int minp = maxp;
   for (int b = 0; b < batch; ++b) {
-    total += pos[b] + 1;
+    total += pos[b];
     minp = std::min(minp, (int)pos[b]);
   }
   const long target = (minp == maxp ? 1 : kRaggedAttnFactor) *

@@ -38,14 +38,15 @@ SMALL = [
                 intermediate=688, rope_base=10000.0, max_seq=3136, pos=(3000,)),
     # one KV head, longer context: 126 splits (more than a wave: the block combine)
     LayerConfig(name="s_kv1_126split", index=15, batch=1, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
-                intermediate=688, rope_base=10000.0, max_seq=8064, pos=(8000,)),
+                intermediate=688, rope_base=10000.0, max_seq=8064, pos=(8001,)),
     # the smallest shapes the ABI takes: hidden 8 (one 16-byte chunk per row), MLP width 8, a
     # one-slot cache (position 0: the step attends only its own new entry)
     LayerConfig(name="s_min", index=16, batch=1, hidden=8, n_heads=1, n_kv_heads=1, head_dim=64,
                 intermediate=8, rope_base=10000.0, max_seq=1, pos=(0,)),
     LayerConfig(name="s_min_b3", index=17, batch=3, hidden=8, n_heads=2, n_kv_heads=1, head_dim=64,
                 intermediate=8, rope_base=10000.0, max_seq=2, pos=(0, 1, 1)),
-    # a 128K-entry context on one KV head: 228 splits (the block combine's loop past its registers)
+    # a 128K-entry context on one KV head: 256 splits, the most a step takes (the block combine's loop
+    # past its registers)
     LayerConfig(name="s_ctx128k", index=20, batch=1, hidden=256, n_heads=1, n_kv_heads=1, head_dim=64,
                 intermediate=688, rope_base=500000.0, max_seq=131136, pos=(131072,)),
     # group 2, batch 9 (two batch tiles of the projections)
