@@ -23,16 +23,16 @@ namespace {
 constexpr uint64_t kLayerMagic = 0x4641535454505331ull;    // "FASTTPS1"
 constexpr uint64_t kWeightsMagic = 0x4641535454505357ull;  // "FASTTPSW"
 constexpr uint64_t kDeadMagic = 0xDEADDEADDEADDEADull;
-// attention blocks per step (256 CUs): 2 per CU for one or two query heads
-// per KV head (each lane with two tiles in flight); one per CU for groups of
-// four (twice the registers per block); four times as many, shorter splits
-// when the batch's positions are ragged. Measured on MI355X: Phi-3 16-sequence
-// ragged batch 101 -> 94 us and GQA 4 x 32768 115 -> 103 us against 768
-// blocks throughout; then 512 blocks with two tiles in flight against 768
-// with one: Phi-3 layer at KV 4096 61.7 -> 61.2 us per step, 16-sequence
-// ragged batch attention 87.9 -> 86.3 us.
+// attention blocks per step (256 CUs): 2 per CU (each lane with two tiles in
+// flight for one or two query heads per KV head, one for groups of four);
+// four times as many, shorter splits when the batch's positions are ragged.
+// Measured on MI355X: Phi-3 16-sequence ragged batch 101 -> 94 us and GQA
+// 4 x 32768 115 -> 103 us against 768 blocks throughout; then 512 blocks with
+// two tiles in flight against 768 with one: Phi-3 layer at KV 4096 61.7 ->
+// 61.2 us per step, 16-sequence ragged batch attention 87.9 -> 86.3 us; and
+// for the GQA layer 512 blocks against 256 (one per CU): 193-195 -> 188-189
+// us per step (384 and 1024 slower).
 constexpr int kTargetAttnBlocks = 512;
-constexpr int kTargetAttnBlocksG4 = 256;
 constexpr int kRaggedAttnFactor = 4;
 constexpr int kAttnTile = 64;
 constexpr int kMaxSplits = 256;
@@ -580,8 +580,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     total += pos[b];
     minp = std::min(minp, (int)pos[b]);
   }
-  const long target = (minp == maxp ? 1 : kRaggedAttnFactor) *
-                      (long)(c.n_heads / c.n_kv_heads >= 4 ? kTargetAttnBlocksG4 : kTargetAttnBlocks);
+  const long target = (minp == maxp ? 1 : kRaggedAttnFactor) * (long)kTargetAttnBlocks;
   int split_len = round_up((int)std::min<long>((total * c.n_kv_heads + target - 1) / target, maxn), kAttnTile);
   split_len = std::max(split_len, round_up(ceil_div(maxn, l->nsplit_cap), kAttnTile));
   const int nsplit = ceil_div(maxn, split_len);
