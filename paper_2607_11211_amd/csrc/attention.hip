@@ -42,7 +42,7 @@
 // split's output (V); the new entry is rounded onto the 8-bit grid once, in
 // double precision, before it is stored and used.
 // A second small kernel combines the splits of each (b, head) with the
-// log-sum-exp identity (one wave per (b, head) up to 64 splits, a block
+// log-sum-exp identity (one wave per (b, head) up to 32 splits, a block
 // beyond). (Cross-block tickets are avoided on purpose: on this
 // chip an agent-scope fence per block costs far more than a kernel boundary.)
 #include "attn_body.h"
@@ -81,12 +81,16 @@ __global__ __launch_bounds__(kThreads) void attn_split_kv8_kernel(AttnArgs a, Kv
 }
 
 // o[b, h] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s,  M = max_s m_s.
-// One block per (head, sequence). Every load is issued up front (the o rows
-// do not depend on M), so the kernel costs one round trip: thread s reads
-// split s's (m, l); thread (group, e) reads o_s[e] of the splits
-// s = group, group + NG, ...
-constexpr int kCombineThreads = 256;
-constexpr int kCombineRegs = 16;  // splits per thread held in registers
+// One block of 1024 threads per (head, sequence), for more than 32 splits.
+// Every load is issued up front (the o rows do not depend on M), so the
+// kernel costs one round trip: thread s reads split s's (m, l); thread
+// (group, e) reads o_s[e] of the splits s = group, group + NG, ... (NG =
+// 1024 / D groups, at most 32 splits each). A 256-thread version that looped
+// over the splits past its registers, one dependent load at a time, took
+// 22 us for 128 splits at d = 128.
+constexpr int kCombineThreads = 1024;
+constexpr int kCombineRegs = 32;  // splits per thread held in registers
+static_assert(kCombineThreads / 128 * kCombineRegs >= kMaxSplits, "one round of loads covers every split");
 
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
@@ -125,8 +129,6 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
       const int q = grp + NG * k;
       if (q < nsplit) acc = fmaf(ov[k], fac[q], acc);
     }
-    for (int q = grp + NG * kCombineRegs; q < nsplit; q += NG)
-      acc = fmaf(ph[(size_t)q * (D + 2) + 2 + e], fac[q], acc);
     osum[grp][e] = acc;
   }
   __syncthreads();
@@ -151,12 +153,14 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
   }
 }
 
-// The same merge by one wave per (head, sequence), for up to 64 splits: lane
-// s reads split s's (m, l); the o values of 32 splits at a time are loaded up
-// front (one round trip for up to 32 splits) and merged with each split's
-// factor read from lane s. No block barrier: on the batch-1 Phi-3 layer this
-// saves ~0.5 us per step against the block version.
-constexpr int kWaveCombineChunk = 32;
+// The same merge by one wave per (head, sequence), for up to 32 splits: lane
+// s reads split s's (m, l); the o values of all splits are loaded up front
+// (one round trip) and merged with each split's factor read from lane s. No
+// block barrier: on the batch-1 Phi-3 layer this saved ~0.5 us per step
+// against a 256-thread block version. Past 32 splits it would need a second
+// round trip, which made it slower than the block kernel (7.2 us for 64
+// splits at d = 128, against 4.9 us for 128 splits in the block kernel).
+constexpr int kWaveCombineSplits = 32;
 template <int D>
 __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* __restrict__ part, int nsplit,
                                                                  int nsplit_cap, int n_heads, float* __restrict__ o,
@@ -168,29 +172,24 @@ __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* _
   const int sl = min(lane, nsplit - 1);
   const float ms = lane < nsplit ? ph[(size_t)sl * (D + 2)] : -INFINITY;
   const float ls = lane < nsplit ? ph[(size_t)sl * (D + 2) + 1] : 0.f;
-  float ov[kWaveCombineChunk][EPL];
-  auto load_chunk = [&](int s0) {
+  float ov[kWaveCombineSplits][EPL];
 #pragma unroll
-    for (int j = 0; j < kWaveCombineChunk; ++j)
+  for (int j = 0; j < kWaveCombineSplits; ++j)
 #pragma unroll
-      for (int i = 0; i < EPL; ++i)
-        ov[j][i] = ph[(size_t)min(s0 + j, nsplit - 1) * (D + 2) + 2 + min(lane + kWave * i, D - 1)];
-  };
-  load_chunk(0);
+    for (int i = 0; i < EPL; ++i)
+      ov[j][i] = ph[(size_t)min(j, nsplit - 1) * (D + 2) + 2 + min(lane + kWave * i, D - 1)];
   const float M = wave_max(ms);
   const float f = merge_factor(ms, M);  // zero for lanes past the splits
   const float L = wave_sum(ls * f);
   float acc[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
-  for (int s0 = 0; s0 < nsplit; s0 += kWaveCombineChunk) {
-    if (s0 > 0) load_chunk(s0);
 #pragma unroll
-    for (int j = 0; j < kWaveCombineChunk; ++j) {
-      const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), s0 + j));
+  for (int j = 0; j < kWaveCombineSplits; ++j) {
+    // lanes past the splits hold f = 0
+    const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j));
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) acc[i] = fmaf(ov[j][i], fj, acc[i]);
-    }
+    for (int i = 0; i < EPL; ++i) acc[i] = fmaf(ov[j][i], fj, acc[i]);
   }
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
@@ -257,7 +256,7 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
 template <int D>
 hipError_t launch_combine_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(a.n_heads, a.batch);
-  if (a.nsplit <= kWave)
+  if (a.nsplit <= kWaveCombineSplits)
     return ext_launch(attn_combine_wave_kernel<D>, grid, dim3(kWave), 0, s, ev, (const float*)a.part, a.nsplit,
                       a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
   return ext_launch(attn_combine_kernel<D>, grid, dim3(kCombineThreads), 0, s, ev, (const float*)a.part, a.nsplit,

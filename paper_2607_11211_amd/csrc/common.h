@@ -137,8 +137,8 @@ __device__ __forceinline__ float wave_max(float v) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
-// Sum of x*x over n bf16 values of a row, for the whole block; every thread
-// gets the total. `red` must hold blockDim.x / 64 floats.
+// Sum of v over the whole block; every thread gets the total. `red` must
+// hold blockDim.x / 64 floats.
 __device__ __forceinline__ float block_sum(float v, float* red) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   v = wave_sum(v);

@@ -33,10 +33,10 @@ SMALL = [
     # GQA group 4, d=128, long base, uneven MLP tile
     LayerConfig(name="s_gqa128", index=12, batch=3, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
                 intermediate=2824, rope_base=500000.0, max_seq=1100, pos=(5, 511, 1000)),
-    # one KV head, long context: 47 splits (the one-wave combine's second chunk of 32)
+    # one KV head, long context: 47 splits (past the one-wave combine's 32: the block combine)
     LayerConfig(name="s_kv1_47split", index=14, batch=1, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=3136, pos=(3000,)),
-    # one KV head, longer context: 126 splits (more than a wave: the block combine)
+    # one KV head, longer context: 126 splits (the block combine, 16 groups of 8 splits at d = 64)
     LayerConfig(name="s_kv1_126split", index=15, batch=1, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=8064, pos=(8001,)),
     # the smallest shapes the ABI takes: hidden 8 (one 16-byte chunk per row), MLP width 8, a
@@ -45,8 +45,19 @@ SMALL = [
                 intermediate=8, rope_base=10000.0, max_seq=1, pos=(0,)),
     LayerConfig(name="s_min_b3", index=17, batch=3, hidden=8, n_heads=2, n_kv_heads=1, head_dim=64,
                 intermediate=8, rope_base=10000.0, max_seq=2, pos=(0, 1, 1)),
-    # a 128K-entry context on one KV head: 256 splits, the most a step takes (the block combine's loop
-    # past its registers)
+    # the two combine kernels at their boundary: 32 splits (one wave) and 33 (a block)
+    LayerConfig(name="s_kv1_32split", index=23, batch=2, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=2112, pos=(2048, 5)),
+    LayerConfig(name="s_kv1_33split", index=24, batch=2, hidden=256, n_heads=4, n_kv_heads=1, head_dim=64,
+                intermediate=688, rope_base=10000.0, max_seq=2112, pos=(2049, 2048)),
+    # the block combine at d = 96 and d = 128 (10 and 8 thread groups per element): 79 splits over
+    # two KV heads, and 141 splits on one KV head with two query heads
+    LayerConfig(name="s_d96_79split", index=21, batch=1, hidden=256, n_heads=2, n_kv_heads=2, head_dim=96,
+                intermediate=688, rope_base=10000.0, max_seq=5056, pos=(5000,)),
+    LayerConfig(name="s_d128_141split", index=22, batch=1, hidden=256, n_heads=2, n_kv_heads=1, head_dim=128,
+                intermediate=688, rope_base=500000.0, max_seq=9024, pos=(9000,)),
+    # a 128K-entry context on one KV head: 256 splits, the most a step takes (every register of the
+    # block combine's threads in use)
     LayerConfig(name="s_ctx128k", index=20, batch=1, hidden=256, n_heads=1, n_kv_heads=1, head_dim=64,
                 intermediate=688, rope_base=500000.0, max_seq=131136, pos=(131072,)),
     # group 2, batch 9 (two batch tiles of the projections)
