@@ -57,12 +57,15 @@ __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
 }
 
 // Launch shape: a batch tile of BT sequences, MAXCH chunks per lane and row
-// segment, NSEG_H segments per half row, NBUF rows in flight per wave (2-4
-// KB: at this size the memory system's queues stay short enough that the
-// waves that start last do not finish much later than the rest).
+// segment, NSEG_H segments per half row, NBUF rows in flight per wave (2-3
+// KB at one sequence, 2-4 KB for batch tiles: at this size the memory
+// system's queues stay short enough that the waves that start last do not
+// finish much later than the rest; the Phi-3 down projection's 2 KB segments
+// one at a time instead of two gave 61.1 -> 60.8 us per layer step, and two
+// or three of the O projection's 3 KB segments instead of one were slower).
 template <int BT, int MAXCH, int NSEG_H, Mode MODE>
 hipError_t launch_shape(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
-  constexpr int NBUF = MAXCH >= 3 ? 1 : 2;
+  constexpr int NBUF = (MAXCH >= 3 || (BT == 1 && MAXCH == 2)) ? 1 : 2;
   const int nblk = a.rows < kNumCu ? a.rows : kNumCu;
   // unsegmented rows add the residual from the register copy only
   constexpr int NG = kWaves / (halves<MODE>() * NSEG_H);
