@@ -153,15 +153,16 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
   }
 }
 
-// The same merge by one wave per (head, sequence), for up to 32 splits: lane
-// s reads split s's (m, l); the o values of all splits are loaded up front
-// (one round trip) and merged with each split's factor read from lane s. No
-// block barrier: on the batch-1 Phi-3 layer this saved ~0.5 us per step
-// against a 256-thread block version. Past 32 splits it would need a second
+// The same merge by one wave per (head, sequence), for up to NS = 16 or 32
+// splits: lane s reads split s's (m, l); the o values of NS splits are loaded
+// up front (one round trip) and merged with each split's factor read from
+// lane s. No block barrier: on the batch-1 Phi-3 layer this saved ~0.5 us per
+// step against a 256-thread block version, and loading 16 splits instead of
+// 32 for its 16 splits another ~0.3 us. Past 32 splits it would need a second
 // round trip, which made it slower than the block kernel (7.2 us for 64
 // splits at d = 128, against 4.9 us for 128 splits in the block kernel).
 constexpr int kWaveCombineSplits = 32;
-template <int D>
+template <int D, int NS>
 __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* __restrict__ part, int nsplit,
                                                                  int nsplit_cap, int n_heads, float* __restrict__ o,
                                                                  uint16_t* __restrict__ o_operand, int o_nbtc) {
@@ -172,9 +173,9 @@ __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* _
   const int sl = min(lane, nsplit - 1);
   const float ms = lane < nsplit ? ph[(size_t)sl * (D + 2)] : -INFINITY;
   const float ls = lane < nsplit ? ph[(size_t)sl * (D + 2) + 1] : 0.f;
-  float ov[kWaveCombineSplits][EPL];
+  float ov[NS][EPL];
 #pragma unroll
-  for (int j = 0; j < kWaveCombineSplits; ++j)
+  for (int j = 0; j < NS; ++j)
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       ov[j][i] = ph[(size_t)min(j, nsplit - 1) * (D + 2) + 2 + min(lane + kWave * i, D - 1)];
@@ -185,7 +186,7 @@ __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* _
 #pragma unroll
   for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
 #pragma unroll
-  for (int j = 0; j < kWaveCombineSplits; ++j) {
+  for (int j = 0; j < NS; ++j) {
     // lanes past the splits hold f = 0
     const float fj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j));
 #pragma unroll
@@ -256,9 +257,12 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
 template <int D>
 hipError_t launch_combine_d(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(a.n_heads, a.batch);
+  if (a.nsplit <= kWaveCombineSplits / 2)
+    return ext_launch(attn_combine_wave_kernel<D, kWaveCombineSplits / 2>, grid, dim3(kWave), 0, s, ev,
+                      (const float*)a.part, a.nsplit, a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
   if (a.nsplit <= kWaveCombineSplits)
-    return ext_launch(attn_combine_wave_kernel<D>, grid, dim3(kWave), 0, s, ev, (const float*)a.part, a.nsplit,
-                      a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
+    return ext_launch(attn_combine_wave_kernel<D, kWaveCombineSplits>, grid, dim3(kWave), 0, s, ev,
+                      (const float*)a.part, a.nsplit, a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
   return ext_launch(attn_combine_kernel<D>, grid, dim3(kCombineThreads), 0, s, ev, (const float*)a.part, a.nsplit,
                     a.nsplit_cap, a.n_heads, a.o, a.o_operand, a.o_nbtc);
 }
