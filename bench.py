@@ -222,30 +222,33 @@ def cpu_baseline(cfg, seconds: float, kv_fmt: str = "bf16"):
 
 
 def read_ceiling(nbytes: int = 4 << 30):
-    """Measured HBM read rate in the same run: the stream-read probe (16-byte
-    loads over 4 GiB, 16 times the Infinity Cache) at a few launch shapes,
-    best of three launches each."""
+    """Measured HBM read rates in the same run: the stream-read probe (16-byte
+    loads over 4 GiB, 16 times the Infinity Cache) at a few launch shapes, best
+    of three launches each, with plain loads and with the non-temporal policy
+    of the weight streams. Returns {flavour: (GB/s, blocks, unroll)}."""
     import ctypes
     import torch
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_11211_amd", "libfasttps_probe.so"))
     lib.fasttps_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
-                                              ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_float)]
+                                              ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                              ctypes.POINTER(ctypes.c_float)]
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     sink = torch.zeros(256, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream().cuda_stream
-    best = None
-    for blocks in (1024, 2048, 4096, 8192):
-        for unroll in (4, 8):
-            for _ in range(3):
-                ms = ctypes.c_float()
-                rc = lib.fasttps_probe_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes,
-                                                   ctypes.c_void_p(sink.data_ptr()), blocks, unroll,
-                                                   ctypes.c_void_p(stream), ctypes.byref(ms))
-                if rc != 0:
-                    raise RuntimeError(f"fasttps_probe_stream_read failed: {rc}")
-                gbps = nbytes / (ms.value * 1e-3) / 1e9
-                if best is None or gbps > best[0]:
-                    best = (gbps, blocks, unroll)
+    best = {}
+    for nt, flavour in ((0, "plain"), (1, "nontemporal")):
+        for blocks in (2048, 4096, 8192):
+            for unroll in (4, 8):
+                for _ in range(3):
+                    ms = ctypes.c_float()
+                    rc = lib.fasttps_probe_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                                       ctypes.c_void_p(sink.data_ptr()), blocks, unroll, nt,
+                                                       ctypes.c_void_p(stream), ctypes.byref(ms))
+                    if rc != 0:
+                        raise RuntimeError(f"fasttps_probe_stream_read failed: {rc}")
+                    gbps = nbytes / (ms.value * 1e-3) / 1e9
+                    if flavour not in best or gbps > best[flavour][0]:
+                        best[flavour] = (gbps, blocks, unroll)
     del buf
     torch.cuda.empty_cache()
     return best
@@ -334,6 +337,212 @@ def sweep(args) -> int:
     return 0
 
 
+def build_workload(cfg, pos, args, kv: str, gemm: str, log_prefix: str = ""):
+    """Resident device copies of a workload: the layers of a stack, or for a
+    single layer a chain of independent copies (own weights and caches)
+    totalling at least 2 GB (at most 32 copies), so that no copy is still in
+    the 256 MB Infinity Cache when the chain comes back to it. Layer 0 comes from the shared input
+    generator (the bits the oracle sample uses), the others are drawn on the
+    device with the same distributions. Returns a dict of handles and buffers."""
+    import torch
+    from paper_2607_11211_amd import inputs
+    from paper_2607_11211_amd import layer as L
+    kv8 = kv != "bf16"
+    kb = kernel_bytes(cfg, pos, 1 if kv8 else 2)
+    step_bytes = kb["fused_layer"]
+    # (a step of a few MB is latency-bound and cached anyway: 32 copies)
+    nl = cfg.layers if cfg.layers > 1 else min(max(1, -(-ROTATE_BYTES // step_bytes)), 32)
+    log(f"{log_prefix}workload {cfg.name}: {nl} layers, batch {cfg.batch}, pos {pos.tolist()[:4]}")
+    gemm_id = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX, "fused": L.GEMM_FUSED}[gemm]
+    lay = L.Layer(cfg, max_batch=max(cfg.batch, 2) if gemm == "matrix" else None)
+    lay.set_gemm_path(gemm_id)
+    weights, kcs, vcs, kss, vss = [], [], [], [], []
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0xFA57 + cfg.index)
+    host0 = inputs.make_layer_inputs(cfg, layer=0, pos=pos)
+    for li in range(nl):
+        if li == 0:
+            w = {k: L.to_device(v) for k, v in host0.weights.items()}
+            if kv8:
+                kc = torch.from_numpy(inputs.make_cache8(cfg, pos, "k", kv)).cuda()
+                vc = torch.from_numpy(inputs.make_cache8(cfg, pos, "v", kv)).cuda()
+            else:
+                kc, vc = L.to_device(host0.k_cache), L.to_device(host0.v_cache)
+        else:
+            w, kc, vc = device_layer(cfg, li, pos, gen, caches=not kv8)
+            if kv8:
+                kc = device_cache8(cfg, pos, "k", kv, gen)
+                vc = device_cache8(cfg, pos, "v", kv, gen)
+        if kv8:
+            kss.append(inputs.make_kv_scales(cfg, "k", kv, layer=li))
+            vss.append(inputs.make_kv_scales(cfg, "v", kv, layer=li))
+        weights.append(lay.pack(w))
+        del w
+        kcs.append(kc)
+        vcs.append(vc)
+    x0 = L.to_device(host0.x)
+    ys = [torch.empty_like(x0) for _ in range(nl)]
+    torch.cuda.synchronize()
+    return dict(cfg=cfg, pos=pos, kv=kv, kb=kb, step_bytes=step_bytes, nl=nl, lay=lay, weights=weights, kcs=kcs,
+                vcs=vcs, kss=kss, vss=vss, x0=x0, ys=ys)
+
+
+def free_workload(wl) -> None:
+    import torch
+    for w in wl["weights"]:
+        w.free()
+    wl["lay"].destroy()
+    wl.clear()
+    torch.cuda.empty_cache()
+
+
+def time_workload(wl, steps: int, warmup: int, graph: bool = True, samples: bool = False):
+    """Times one decode step (every layer of the workload once) with stream
+    launches and as a HIP-graph replay (checked to reproduce the eager result
+    bit for bit on three replays with eager steps in between), and the
+    kernels' own durations from events stamped by their dispatches."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    lay, nl, pos, kv = wl["lay"], wl["nl"], wl["pos"], wl["kv"]
+    weights, kcs, vcs, kss, vss, x0, ys = (wl[k] for k in ("weights", "kcs", "vcs", "kss", "vss", "x0", "ys"))
+    stream = torch.cuda.current_stream()
+
+    def layer_step(li, x, s_):
+        if kv != "bf16":
+            lay.step_kv8(weights[li], kv, x, pos, kcs[li], vcs[li], kss[li], vss[li], ys[li], s_)
+        else:
+            lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], s_)
+
+    def step():
+        x = x0
+        for li in range(nl):
+            layer_step(li, x, stream)
+            x = ys[li]
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    y_ref = L.from_device(ys[-1])
+    out = {}
+    # K decode steps launched on the stream
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    e1.synchronize()
+    out["stream_ms"] = e0.elapsed_time(e1) / steps
+    # per-kernel durations over K more steps (the stamping costs host time per
+    # launch, so it stays out of the timed steps above)
+    nprof = min(steps * nl, 1 << 16)
+    lay.profile_begin(nprof)
+    for _ in range(steps):
+        step()
+    kms = lay.profile_end(nprof)
+    names = L.kernel_names()
+    out["kern_us"] = {n: float(np.mean(kms[:, i]) * 1e3) for i, n in enumerate(names) if np.any(kms[:, i] > 0)}
+    out["graph_ms"] = None
+    out["step_samples"] = None
+    if graph:
+        try:
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(stream)
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    x = x0
+                    for li in range(nl):
+                        layer_step(li, x, s)
+                        x = ys[li]
+            stream.wait_stream(s)
+            torch.cuda.synchronize()
+            ok = True
+            for _ in range(3):  # replays must match the eager result
+                g.replay()
+                torch.cuda.synchronize()
+                ok &= bool(np.array_equal(L.from_device(ys[-1]), y_ref))
+                step()
+                torch.cuda.synchronize()
+            if not ok:
+                log("graph replay disagrees with eager steps; graph timing dropped")
+            else:
+                for _ in range(warmup):
+                    g.replay()
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for _ in range(steps):
+                    g.replay()
+                e1.record(stream)
+                e1.synchronize()
+                out["graph_ms"] = e0.elapsed_time(e1) / steps
+                if samples:
+                    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                           for _ in range(steps)]
+                    for a0, a1 in evs:
+                        a0.record(stream)
+                        g.replay()
+                        a1.record(stream)
+                    torch.cuda.synchronize()
+                    out["step_samples"] = np.array([a0.elapsed_time(a1) for a0, a1 in evs])
+            del g
+        except Exception as ex:  # capture unsupported: report stream timing only
+            log(f"graph capture failed: {ex!r}")
+    ms = min(out["stream_ms"], out["graph_ms"]) if out["graph_ms"] is not None else out["stream_ms"]
+    out["ms_step"] = ms
+    out["us_layer"] = ms * 1e3 / nl
+    out["gbps"] = wl["step_bytes"] / (out["us_layer"] * 1e-6) / 1e9
+    return out
+
+
+def dominant_roofline(kb, kern_us):
+    dominant = max(kern_us, key=kern_us.get)
+    ach = kb[dominant] / (kern_us[dominant] * 1e-6) / 1e9 if kb[dominant] else None
+    return {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1) if ach else None,
+            "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBPS, 4) if ach else None,
+            "traffic": load_traffic(dominant), "algorithmic_bytes": kb[dominant],
+            "avg_launch_us": round(kern_us[dominant], 3)}
+
+
+# the other workloads timed in the default run (each a chain of rotating
+# copies; per layer step)
+OTHER_WORKLOADS = ("tiny", "phi3_kv1k", "phi3_batch16_ragged", "gqa_longctx")
+
+
+def other_workloads(args):
+    """Per-layer-step figures of the other workloads, measured in the same run
+    with a bounded number of steps."""
+    from paper_2607_11211_amd import configs, inputs
+    res = {}
+    for name in OTHER_WORKLOADS:
+        cfg = configs.get(name)
+        pos = inputs.make_pos(cfg)
+        cfg = cfg.with_pos(pos)
+        wl = build_workload(cfg, pos, args, "bf16", "auto", log_prefix="  ")
+        t = time_workload(wl, steps=max(5, min(args.steps, 20)), warmup=3)
+        kb, kern = wl["kb"], t["kern_us"]
+        dom = max(kern, key=kern.get)
+        entry = {"us_per_layer": round(t["us_layer"], 3),
+                 "us_per_layer_graph": round(t["graph_ms"] * 1e3 / wl["nl"], 3) if t["graph_ms"] else None,
+                 "us_per_layer_stream": round(t["stream_ms"] * 1e3 / wl["nl"], 3),
+                 "bytes_per_layer_step": wl["step_bytes"], "batch": cfg.batch,
+                 "kv_entries": [int(p) for p in pos], "rotating_copies": wl["nl"],
+                 "kernels_us": {k: round(v, 3) for k, v in kern.items()},
+                 "dominant_kernel": dom}
+        if name == "tiny":
+            entry["note"] = "1.7 MB per step: launch- and latency-bound, no roofline claim"
+        else:
+            entry["hbm_gbps"] = round(t["gbps"], 1)
+            entry["hbm_frac_of_peak"] = round(t["gbps"] / PEAK_HBM_GBPS, 4)
+            entry["dominant_kernel_gbps"] = round(kb[dom] / (kern[dom] * 1e-6) / 1e9, 1) if kb[dom] else None
+        log(f"  {name}: {entry['us_per_layer']} us per layer step"
+            + (f", {entry.get('hbm_gbps')} GB/s" if "hbm_gbps" in entry else "")
+            + f"; kernels " + ", ".join(f"{k} {v:.2f}" for k, v in kern.items()))
+        res[name] = entry
+        free_workload(wl)
+    return res
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -343,6 +552,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip timing the other workloads (tiny, Phi-3 at KV 1024, the 16-sequence ragged batch, "
+                         "the long-context GQA layer) after the headline one")
     ap.add_argument("--sweep", action="store_true",
                     help="latency sweeps over the context length and the head dimension (fused vs op-by-op), "
                          "one JSON line per point, instead of the benchmark")
@@ -392,144 +604,25 @@ def main() -> int:
             print("bench.py: the one-kernel step reads a bf16 cache only", file=sys.stderr)
             return 2
         text += f"; 8-bit KV cache ({args.kv} codes, one scale per KV head)"
-    kb = kernel_bytes(cfg, pos, 1 if kv8 else 2)
-    step_bytes = kb["fused_layer"]
-    # a single-layer workload runs as a chain of independent copies (own
-    # weights and caches) totalling at least 2 GB, so that no copy is still
-    # in the 256 MB Infinity Cache when the chain comes back to it
-    nl = cfg.layers if cfg.layers > 1 else max(1, -(-ROTATE_BYTES // step_bytes))
-    log(f"workload {cfg.name}: {nl} layers, batch {cfg.batch}, pos {pos.tolist()[:4]}")
 
-    gemm = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX, "fused": L.GEMM_FUSED}[args.gemm]
-    lay = L.Layer(cfg, max_batch=max(cfg.batch, 2) if args.gemm == "matrix" else None)
-    lay.set_gemm_path(gemm)
-    weights, kcs, vcs, kss, vss = [], [], [], [], []
-    gen = torch.Generator(device="cuda")
-    gen.manual_seed(0xFA57 + cfg.index)
-    host0 = inputs.make_layer_inputs(cfg, layer=0, pos=pos)
-    for li in range(nl):
-        if li == 0:
-            w = {k: L.to_device(v) for k, v in host0.weights.items()}
-            if kv8:
-                kc = torch.from_numpy(inputs.make_cache8(cfg, pos, "k", args.kv)).cuda()
-                vc = torch.from_numpy(inputs.make_cache8(cfg, pos, "v", args.kv)).cuda()
-            else:
-                kc, vc = L.to_device(host0.k_cache), L.to_device(host0.v_cache)
-        else:
-            w, kc, vc = device_layer(cfg, li, pos, gen, caches=not kv8)
-            if kv8:
-                kc = device_cache8(cfg, pos, "k", args.kv, gen)
-                vc = device_cache8(cfg, pos, "v", args.kv, gen)
-        if kv8:
-            kss.append(inputs.make_kv_scales(cfg, "k", args.kv, layer=li))
-            vss.append(inputs.make_kv_scales(cfg, "v", args.kv, layer=li))
-        weights.append(lay.pack(w))
-        del w
-        kcs.append(kc)
-        vcs.append(vc)
-    x0 = L.to_device(host0.x)
-    ys = [torch.empty_like(x0) for _ in range(nl)]
-    torch.cuda.synchronize()
+    wl = build_workload(cfg, pos, args, args.kv, args.gemm)
+    nl, kb, step_bytes = wl["nl"], wl["kb"], wl["step_bytes"]
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.2f} GiB via torch + packed weights")
-
-    stream = torch.cuda.current_stream()
-
-    def layer_step(li, x, s_):
-        if kv8:
-            lay.step_kv8(weights[li], args.kv, x, pos, kcs[li], vcs[li], kss[li], vss[li], ys[li], s_)
-        else:
-            lay.step(weights[li], x, pos, kcs[li], vcs[li], ys[li], s_)
-
-    def step():
-        x = x0
-        for li in range(nl):
-            layer_step(li, x, stream)
-            x = ys[li]
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    y_ref = L.from_device(ys[-1])
-
-    # timed region: K decode steps on the stream
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    e1.synchronize()
-    stream_ms = e0.elapsed_time(e1) / args.steps
+    t = time_workload(wl, args.steps, args.warmup, graph=not args.no_graph, samples=True)
+    stream_ms, graph_ms, kern_us = t["stream_ms"], t["graph_ms"], t["kern_us"]
     log(f"stream: {stream_ms:.3f} ms/step, {stream_ms * 1e3 / nl:.2f} us/layer")
-
-    # per-kernel durations over K more steps on the same stream, each kernel
-    # bracketed by HIP events stamped at its own dispatch (the stamping costs
-    # host time per launch, so it stays out of the timed steps above)
-    nprof = min(args.steps * nl, 1 << 16)
-    lay.profile_begin(nprof)
-    for _ in range(args.steps):
-        step()
-    kms = lay.profile_end(nprof)
-    log(f"per-kernel events over {kms.shape[0]} layer steps")
-    names = L.kernel_names()
-    # kernels the step launched (the others read 0)
-    kern_us = {n: float(np.mean(kms[:, i]) * 1e3) for i, n in enumerate(names) if np.any(kms[:, i] > 0)}
     log("kernels (us): " + ", ".join(f"{n} {v:.2f}" for n, v in kern_us.items()))
-
-    # HIP-graph replay of the whole decode step
-    graph_ms = None
-    step_samples = None
-    if not args.no_graph:
-        try:
-            g = torch.cuda.CUDAGraph()
-            s = torch.cuda.Stream()
-            s.wait_stream(stream)
-            with torch.cuda.stream(s):
-                with torch.cuda.graph(g, stream=s):
-                    x = x0
-                    for li in range(nl):
-                        layer_step(li, x, s)
-                        x = ys[li]
-            stream.wait_stream(s)
-            torch.cuda.synchronize()
-            ok = True
-            for _ in range(3):  # replays must match the eager result
-                g.replay()
-                torch.cuda.synchronize()
-                ok &= bool(np.array_equal(L.from_device(ys[-1]), y_ref))
-                step()
-                torch.cuda.synchronize()
-            if not ok:
-                log("graph replay disagrees with eager steps; graph timing dropped")
-            else:
-                for _ in range(args.warmup):
-                    g.replay()
-                torch.cuda.synchronize()
-                e0.record(stream)
-                for _ in range(args.steps):
-                    g.replay()
-                e1.record(stream)
-                e1.synchronize()
-                graph_ms = e0.elapsed_time(e1) / args.steps
-                log(f"graph: {graph_ms:.3f} ms/step, {graph_ms * 1e3 / nl:.2f} us/layer")
-                # the spread over single steps (events around each replay)
-                evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                       for _ in range(args.steps)]
-                for a0, a1 in evs:
-                    a0.record(stream)
-                    g.replay()
-                    a1.record(stream)
-                torch.cuda.synchronize()
-                step_samples = np.array([a0.elapsed_time(a1) for a0, a1 in evs])
-        except Exception as ex:  # capture unsupported: report stream timing only
-            log(f"graph capture failed: {ex!r}")
-            graph_ms = None
+    if graph_ms is not None:
+        log(f"graph: {graph_ms:.3f} ms/step, {graph_ms * 1e3 / nl:.2f} us/layer")
+    step_samples = t["step_samples"]
 
     # the op-by-op baseline on the same workload, replayed as a HIP graph
     unfused = None
     if kv8 and not args.no_unfused:
         log("op-by-op baseline: not built for an 8-bit cache; skipped")
     if not args.no_unfused and not kv8:
+        lay, weights, kcs, vcs, x0, ys = (wl[k] for k in ("lay", "weights", "kcs", "vcs", "x0", "ys"))
+        stream = torch.cuda.current_stream()
         lay.enable_unfused()
         yu = [torch.empty_like(x0) for _ in range(nl)]
 
@@ -552,6 +645,7 @@ def main() -> int:
         for _ in range(2):
             gu.replay()
         torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(args.steps):
             gu.replay()
@@ -562,23 +656,23 @@ def main() -> int:
         unfused = {"us_per_layer": round(unf_ms * 1e3 / nl, 3), "ms_per_step": round(unf_ms, 4),
                    "launches_per_layer": 24, "y_bitwise_equal_to_fused": same}
         log(f"unfused baseline (graph): {unf_ms:.3f} ms/step, {unf_ms * 1e3 / nl:.2f} us/layer")
-        del gu
+        del gu, yu
+    free_workload(wl)
 
-    ms_step = min(stream_ms, graph_ms) if graph_ms is not None else stream_ms
-    us_layer = ms_step * 1e3 / nl
-    gbps = step_bytes / (us_layer * 1e-6) / 1e9
+    ms_step, us_layer, gbps = t["ms_step"], t["us_layer"], t["gbps"]
+    roofline = dominant_roofline(kb, kern_us)
 
-    dominant = max(kern_us, key=kern_us.get)
-    ach = kb[dominant] / (kern_us[dominant] * 1e-6) / 1e9 if kb[dominant] else None
-    traffic = load_traffic(dominant)
-    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(ach, 1) if ach else None,
-                "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBPS, 4) if ach else None,
-                "traffic": traffic, "algorithmic_bytes": kb[dominant],
-                "avg_launch_us": round(kern_us[dominant], 3)}
-
-    ceiling, c_blocks, c_unroll = read_ceiling()
-    log(f"read ceiling (stream-read probe, 4 GiB): {ceiling:.0f} GB/s at {c_blocks} blocks, unroll {c_unroll}")
+    ceil = read_ceiling()
+    for fl, (g_, b_, u_) in ceil.items():
+        log(f"read ceiling (stream-read probe, 4 GiB, {fl} loads): {g_:.0f} GB/s at {b_} blocks, unroll {u_}")
+    ceiling, c_blocks, c_unroll = ceil["nontemporal"]
     wbytes = cfg.weight_bytes()
+
+    workloads = None
+    if not args.no_workloads and args.workload == "phi3_stack32_kv4k" and args.batch is None and not kv8 \
+            and args.gemm == "auto":
+        log("other workloads (per layer step, rotating copies, HIP-graph replay)")
+        workloads = other_workloads(args)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -599,8 +693,9 @@ def main() -> int:
         "gemm_path": args.gemm, "kv_cache": args.kv,
         "hbm_gbps": round(gbps, 1), "hbm_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "read_ceiling": {"gbps": round(ceiling, 1),
-                         "method": f"libfasttps_probe stream read of 4 GiB with 16-byte loads, best launch "
-                                   f"({c_blocks} blocks x 256 threads, {c_unroll} loads in flight per thread)",
+                         "method": f"libfasttps_probe stream read of 4 GiB with 16-byte non-temporal loads, best "
+                                   f"launch ({c_blocks} blocks x 256 threads, {c_unroll} loads in flight per thread)",
+                         "plain_loads_gbps": round(ceil["plain"][0], 1),
                          "layer_frac_of_ceiling": round(gbps / ceiling, 4)},
         "weights_only_gbps": round(wbytes / (us_layer * 1e-6) / 1e9, 1),
         "us_per_layer_p10_p50_p90": ([round(float(np.percentile(step_samples, q)) * 1e3 / nl, 3)
@@ -612,6 +707,7 @@ def main() -> int:
         "roofline": roofline,
         "unfused_baseline": (dict(unfused, speedup_of_fused=round(unfused["us_per_layer"] / us_layer, 3))
                              if unfused else None),
+        "workloads": workloads,
         "cpu_baseline": cpu,
     }
     if args.calibrate_copy:

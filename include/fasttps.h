@@ -110,9 +110,14 @@ FASTTPS_API int fasttps_weights_pack(fasttps_layer* layer, const fasttps_weights
  *   k_cache, v_cache
  *            device, [batch, H_kv, N_max, d] bf16 (a leading block of a
  *            [B_max, ...] cache is fine). Entries [0, pos[b]) are read; the
- *            one slot pos[b] of every (b, g) is written; nothing else is read
- *            or written. After the call the caller's length is pos[b] + 1
- *            (Section 3.1.1: N_p <- N_p + 1, N_r <- N_r - 1).
+ *            one slot pos[b] of every (b, g) is written; nothing else is
+ *            written. Nothing else is read either, with one exception: a
+ *            sequence with pos[b] = 0 has no cached entry, and the attention's
+ *            loads, issued ahead of their use and clamped to entry
+ *            max(pos[b] - 1, 0), then read slot 0 before or while it is being
+ *            written and discard the values. After the call the caller's
+ *            length is pos[b] + 1 (Section 3.1.1 GKVC: N_p <- N_p + 1,
+ *            N_r <- N_r - 1).
  *   y        device, [batch, D] bf16 output; must not overlap x or the caches
  *   stream   the step is enqueued on this stream; the call neither allocates
  *            nor synchronizes.
@@ -213,11 +218,19 @@ FASTTPS_API int fasttps_set_attention_p_bf16(fasttps_layer* layer, int32_t enabl
 /* Test hook: copy one of the step's fp32 intermediates from the handle's
  * scratch into `dst` (device), on `stream`, after a fasttps_decode_step on the
  * same stream. `which` selects:
- *   FASTTPS_DBG_QKV   [batch, (H + 2 H_kv) d]  q | k | v before RoPE
- *   FASTTPS_DBG_ATTN  [batch, H d]             attention output o
- *   FASTTPS_DBG_H1    [batch, D]               x + W_o o
- *   FASTTPS_DBG_MLP_A [batch, K]               SiLU(gate) * up (h^sm of Alg. 4)
- * `bytes` must equal the size of the selected buffer for `batch`. */
+ *   FASTTPS_DBG_QKV     [batch, (H + 2 H_kv) d]  q | k | v before RoPE
+ *   FASTTPS_DBG_ATTN    [batch, H d]             attention output o
+ *   FASTTPS_DBG_H1      [batch, D]               x + W_o o
+ *   FASTTPS_DBG_MLP_A   [batch, K]               SiLU(gate) * up (h^sm of Alg. 4)
+ *   FASTTPS_DBG_QK_ROPE [batch, (H + H_kv) d]    q | k after the joint RoPE (Alg. 3,
+ *                                                Eq. 22), before k is rounded for the cache
+ *   FASTTPS_DBG_H       [batch, D]               RMSNorm1(x), the QKV projection's input
+ *   FASTTPS_DBG_H2      [batch, D]               RMSNorm2(h1), the gate/up projection's input
+ * The last three are written only by steps taken while fasttps_set_debug is
+ * on (QK_ROPE by the vector and matrix-core paths, H and H2 by the vector
+ * path); reading one the last step did not write fails with
+ * FASTTPS_ERR_INVALID_ARG. `bytes` must equal the size of the selected
+ * buffer for `batch`. */
 #define FASTTPS_DBG_QKV   0
 #define FASTTPS_DBG_ATTN  1
 #define FASTTPS_DBG_H1    2
@@ -225,8 +238,34 @@ FASTTPS_API int fasttps_set_attention_p_bf16(fasttps_layer* layer, int32_t enabl
 #define FASTTPS_DBG_FUSED_WAITS 4  /* int32 [1]: bounded waits of the fused kernel that ran
                                       out since the layer was created (0 when every phase
                                       hand-over completed); `batch` is ignored */
+#define FASTTPS_DBG_QK_ROPE 5
+#define FASTTPS_DBG_H       6
+#define FASTTPS_DBG_H2      7
 FASTTPS_API int fasttps_debug_read(fasttps_layer* layer, int32_t which, int32_t batch, void* dst,
                        size_t bytes, void* stream);
+
+/* Test hook: when enabled, later steps of this handle also write the
+ * intermediates FASTTPS_DBG_QK_ROPE, FASTTPS_DBG_H and FASTTPS_DBG_H2 (a few
+ * KB per sequence, after each kernel's weight or cache stream) into the
+ * handle's scratch. Off by default. */
+FASTTPS_API int fasttps_set_debug(fasttps_layer* layer, int32_t enable);
+
+/* The argument checks of fasttps_decode_step (cache_elem_bytes 2) or
+ * fasttps_decode_step_kv8 (cache_elem_bytes 1) against a layer config,
+ * without a handle and without any HIP call: the status a step with these
+ * arguments returns before its first launch (handle checks aside).
+ *   cfg          host; validated as by fasttps_layer_create
+ *   x, k_cache, v_cache, y
+ *                only their addresses are examined (null, 16-byte
+ *                alignment, overlap); nothing is dereferenced
+ *   pos          host, [batch] int32, read
+ * Returns FASTTPS_OK, FASTTPS_ERR_INVALID_ARG (null pointer, batch outside
+ * [1, max_batch], y overlapping x or a cache, the caches overlapping),
+ * FASTTPS_ERR_ALIGNMENT, FASTTPS_ERR_CACHE_FULL (a pos[b] outside
+ * [0, N_max)) or a config error. */
+FASTTPS_API int fasttps_validate_step(const fasttps_config* cfg, const void* x, const int32_t* pos,
+                                      int32_t batch, const void* k_cache, const void* v_cache, const void* y,
+                                      int32_t cache_elem_bytes);
 
 /* Measurement hook: time every kernel of the next `max_steps` steps of this
  * handle. Each kernel of those steps is launched with start/stop events that

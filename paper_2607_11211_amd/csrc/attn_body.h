@@ -139,7 +139,12 @@ __device__ __forceinline__ void store_new(uint8_t* row, int e, double x, double 
 }
 
 // This lane's K and V chunks of the tile at t0: position t0 + j (clamped to
-// `last`, a position of this split), quarter `seg` of the row.
+// `last`, a position of this split), quarter `seg` of the row. Plain loads:
+// the three chunks of a lane's quarter row are three load instructions, and
+// each of them touches every 128-byte line of the 16 rows the wave reads, so
+// the lines must stay in L2 between them; with the non-temporal policy of the
+// weight streams the Phi-3 attention at KV 4096 took 15.0 instead of 11.4 us
+// on MI355X.
 template <int ROW_CHUNKS, int NC, typename Chunk>
 __device__ __forceinline__ void tile_load(Chunk (&k)[NC], Chunk (&v)[NC], const Chunk* __restrict__ Kc,
                                           const Chunk* __restrict__ Vc, int t0, int last, int j, int seg) {
@@ -197,7 +202,8 @@ struct AttnBody {
     start = s * kTile;
     stride = a.nsplit * kTile;
     end = live ? P : start;
-    last = P;  // loads past the end read this row (masked)
+    last = max(P - 1, 0);  // loads past the end read this cached row (masked); slot P is never read
+                           // unless P = 0, where the clamped prime loads read slot 0 and discard it
     head_off = ((size_t)b * a.n_kv_heads + g) * (size_t)a.max_seq * D * kv_bytes<KVF>();  // bytes
     Kc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.k_cache) + head_off);
     Vc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.v_cache) + head_off);
@@ -332,6 +338,23 @@ struct AttnBody {
         decode_chunk<KVF>(reinterpret_cast<const Chunk*>(sm.vnew)[seg * NC + c], vf + R::EPC * c);
       }
       update(kf, vf, true);
+    }
+
+    // test hook: q and k after RoPE (fp32), written after the stream by the
+    // split that owns the new entry
+    if (a.dbg_qk && own_new) {
+      const int H = a.n_heads, Hkv = a.n_kv_heads;
+      float* dq = a.dbg_qk + (size_t)b * (H + Hkv) * D;
+      for (int i = tid; i < G * D; i += kThreads) dq[(size_t)g * G * D + i] = sm.q[i / D][i % D];
+      if (tid < HALF) {
+        // k and its cos/sin row again from memory (not held across the loop)
+        const size_t kg = (size_t)b * (H + 2 * Hkv) * D + (size_t)H * D + (size_t)g * D;
+        const double kk0 = a.qkv[kg + pj], kk1 = a.qkv[kg + pj + HALF];
+        const double c = a.rope_cos[(size_t)P * HALF + pj], sn = a.rope_sin[(size_t)P * HALF + pj];
+        float* dk = dq + (size_t)H * D + (size_t)g * D;
+        dk[pj] = (float)(kk0 * c - kk1 * sn);
+        dk[pj + HALF] = (float)(kk1 * c + kk0 * sn);
+      }
     }
 
     // ---- merge: the 4 positions of each 16-lane row (DPP), then the rows --

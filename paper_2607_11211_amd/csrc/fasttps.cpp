@@ -110,7 +110,11 @@ constexpr int kMfmaWaves = 16;  // waves per block of the MFMA kernels (they spl
 // intermediate unit is one contiguous 2D-value row for the projection kernel.
 constexpr int kInterlaceTile = 1;
 
+// test-hook buffers a step wrote (fasttps_layer::dbg_written)
+constexpr int kDbgQk = 1, kDbgNorm = 2;
+
 }  // namespace
+
 
 struct fasttps_layer {
   uint64_t magic;
@@ -118,6 +122,10 @@ struct fasttps_layer {
   int device;
   int nsplit_cap;
   int p_bf16 = 0;  // accuracy study switch (fasttps_set_attention_p_bf16)
+  int debug = 0;   // test hook switch (fasttps_set_debug)
+  // what the last step wrote to the test-hook buffers: kDbgQk (q, k after
+  // RoPE), kDbgNorm (the two normalized activations; vector path only)
+  int dbg_written = 0;
   void* arena;
   double* rope_cos;
   double* rope_sin;
@@ -126,6 +134,11 @@ struct fasttps_layer {
   float* attn_o;
   float* h1;
   float* mlp_a;
+  // test-hook outputs: q | k after RoPE [B, (H + H_kv) d], RMSNorm1(x) and
+  // RMSNorm2(h1) [B, D]
+  float* dbg_qk;
+  float* dbg_h;
+  float* dbg_h2;
   // operands of the MFMA projections (layers with max_batch > 1): o, h1 * gamma2
   // and SiLU(g) * u split into bf16 levels in lane order, and RMSNorm2's
   // per-stripe sums of squares
@@ -280,7 +293,7 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   const bool mfma = B > 1;
   const int nbtc = 2 * ceil_div(B, 16);
   const LayerTiles lt = layer_tiles(c);
-  size_t sizes[12] = {
+  size_t sizes[15] = {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
@@ -293,9 +306,12 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
       mfma ? (size_t)lt.down.kt * nbtc * 512 * sizeof(uint16_t) : 0,
       mfma ? (size_t)lt.o.ns * B * sizeof(float) : 0,
       (size_t)kFusedPhases * kFusedBlocks * sizeof(unsigned) + 2 * sizeof(unsigned),
+      (size_t)B * (c.n_heads + c.n_kv_heads) * d * sizeof(float),
+      (size_t)B * c.hidden * sizeof(float),
+      (size_t)B * c.hidden * sizeof(float),
   };
-  size_t total = 0, offs[12];
-  for (int i = 0; i < 12; ++i) {
+  size_t total = 0, offs[15];
+  for (int i = 0; i < 15; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -338,6 +354,9 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   l->fused_flags = reinterpret_cast<unsigned*>(base + offs[11]);
   l->fused_epoch = l->fused_flags + kFusedPhases * kFusedBlocks;
   l->fused_err = reinterpret_cast<int*>(l->fused_epoch + 1);
+  l->dbg_qk = reinterpret_cast<float*>(base + offs[12]);
+  l->dbg_h = reinterpret_cast<float*>(base + offs[13]);
+  l->dbg_h2 = reinterpret_cast<float*>(base + offs[14]);
 
   // the operand buffers start at zero: their padding (inputs past the
   // matrix's last column) must stay zero, since the padded weights are zero
@@ -517,15 +536,10 @@ int fasttps_weights_free(fasttps_weights* w) {
 
 namespace {
 
-// The checks shared by both step entry points; on success *maxp is the largest
-// position of the batch. Makes no HIP call.
-int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
-               void* k_cache, void* v_cache, void* y, int* maxp, size_t cache_elem_bytes = 2) {
-  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
-  if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad weights handle");
-  const fasttps_config& c = l->cfg;
-  if (!same_shape(c, w->cfg))
-    return fail(FASTTPS_ERR_BAD_HANDLE, "weights were packed for another layer shape");
+// The argument checks of a step against a layer config (no handle, no HIP
+// call); on success *maxp is the largest position of the batch.
+int check_args(const fasttps_config& c, const void* x, const int32_t* pos, int32_t batch, const void* k_cache,
+               const void* v_cache, const void* y, int* maxp, size_t cache_elem_bytes) {
   if (!x || !pos || !k_cache || !v_cache || !y) return fail(FASTTPS_ERR_INVALID_ARG, "null pointer argument");
   if (batch < 1 || batch > c.max_batch)
     return fail(FASTTPS_ERR_INVALID_ARG, "batch %d outside [1, %d]", batch, c.max_batch);
@@ -549,30 +563,40 @@ int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const 
   return FASTTPS_OK;
 }
 
+// The checks shared by the step entry points: the handles, then the
+// arguments. Makes no HIP call.
+int check_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
+               void* k_cache, void* v_cache, void* y, int* maxp, size_t cache_elem_bytes = 2) {
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (!weights_ok(w)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad weights handle");
+  if (!same_shape(l->cfg, w->cfg))
+    return fail(FASTTPS_ERR_BAD_HANDLE, "weights were packed for another layer shape");
+  return check_args(l->cfg, x, pos, batch, k_cache, v_cache, y, maxp, cache_elem_bytes);
+}
+
 }  // namespace
+
+int fasttps_validate_step(const fasttps_config* cfg, const void* x, const int32_t* pos, int32_t batch,
+                          const void* k_cache, const void* v_cache, const void* y, int32_t cache_elem_bytes) {
+  g_last_error.clear();
+  int st = validate_config(cfg);
+  if (st) return st;
+  if (cache_elem_bytes != 1 && cache_elem_bytes != 2)
+    return fail(FASTTPS_ERR_INVALID_ARG, "cache_elem_bytes %d: 2 (bf16) or 1 (8-bit codes)", cache_elem_bytes);
+  int maxp = 0;
+  return check_args(*cfg, x, pos, batch, k_cache, v_cache, y, &maxp, (size_t)cache_elem_bytes);
+}
 
 }  // extern "C"
 
 namespace {
 
-// The fused step after validation: kvf is the cache format (kKvBf16, or an
-// 8-bit format with its scales in *sc).
-int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
-             void* k_cache, void* v_cache, void* y, void* stream, int maxp, int kvf, const KvScales* sc) {
+// Attention split: the tiles of 64 cached positions [0, pos) of every
+// (sequence, kv head) are dealt to nsplit interleaved splits of about
+// split_len positions, so that about `target` blocks carry the work (the new
+// entry at pos comes from registers, so it adds no tile of its own).
+int attention_splits(const fasttps_layer* l, const int32_t* pos, int32_t batch, int maxp) {
   const fasttps_config& c = l->cfg;
-  const size_t D = c.hidden, d = c.head_dim;
-  // projections on the matrix cores from kMfmaMinBatch sequences up (or as
-  // fasttps_set_gemm_path says), where the weights carry MFMA tiles
-  const bool have_tiles = w->t_qkv != nullptr && l->op_o != nullptr;
-  const bool mfma = l->gemm_path == FASTTPS_GEMM_MATRIX ||
-                    (l->gemm_path == FASTTPS_GEMM_AUTO && have_tiles && batch >= kMfmaMinBatch);
-  if (mfma && !have_tiles)
-    return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
-
-  // attention split: the tiles of 64 cached positions [0, pos) of every
-  // (sequence, kv head) are dealt to nsplit interleaved splits of about
-  // split_len positions, so that about `target` blocks carry the work (the
-  // new entry at pos comes from registers, so it adds no tile of its own)
   const int maxn = std::max(maxp, 1);
   long total = 0;
   int minp = maxp;
@@ -583,7 +607,40 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   const long target = (minp == maxp ? 1 : kRaggedAttnFactor) * (long)kTargetAttnBlocks;
   int split_len = round_up((int)std::min<long>((total * c.n_kv_heads + target - 1) / target, maxn), kAttnTile);
   split_len = std::max(split_len, round_up(ceil_div(maxn, l->nsplit_cap), kAttnTile));
-  const int nsplit = ceil_div(maxn, split_len);
+  return ceil_div(maxn, split_len);
+}
+
+// Where a step keeps its fp32 intermediates (by default the layer handle's
+// scratch).
+struct StepScratch {
+  float* qkv;
+  float* part;
+  float* o;
+  float* h1;
+  float* a;
+  int nsplit_cap;
+  bool noalloc;  // scratch not owned by the handle: the vector path only, no test hooks, no timing events
+};
+
+// The fused step after validation: kvf is the cache format (kKvBf16, or an
+// 8-bit format with its scales in *sc); scr overrides the layer's scratch.
+int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos, int32_t batch,
+             void* k_cache, void* v_cache, void* y, void* stream, int maxp, int kvf, const KvScales* sc,
+             const StepScratch* scr = nullptr) {
+  const fasttps_config& c = l->cfg;
+  const size_t D = c.hidden, d = c.head_dim;
+  const StepScratch own{l->qkv, l->attn_part, l->attn_o, l->h1, l->mlp_a, l->nsplit_cap, false};
+  const StepScratch& S = scr ? *scr : own;
+  // projections on the matrix cores from kMfmaMinBatch sequences up (or as
+  // fasttps_set_gemm_path says), where the weights carry MFMA tiles; the
+  // allocation-free step runs the vector path
+  const bool have_tiles = w->t_qkv != nullptr && l->op_o != nullptr;
+  const bool mfma = !S.noalloc && (l->gemm_path == FASTTPS_GEMM_MATRIX ||
+                                   (l->gemm_path == FASTTPS_GEMM_AUTO && have_tiles && batch >= kMfmaMinBatch));
+  if (mfma && !have_tiles)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
+
+  const int nsplit = attention_splits(l, pos, batch, maxp);
 
   // one sequence: the whole step as one persistent kernel, on request
   // (FASTTPS_GEMM_FUSED), where it is built for the shape and the step is the
@@ -599,7 +656,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   fsh.down = gemv_shape_b1(c.intermediate, false);
   const bool fused_ok = batch == 1 && kvf == kKvBf16 && l->p_bf16 == 0 && nsplit <= 64 &&
                         ceil_div(c.n_heads * (int)d, kFusedBlocks) * nsplit <= 1024 && fused_layer_supported(fsh);
-  const bool fused = !mfma && l->gemm_path == FASTTPS_GEMM_FUSED;
+  const bool fused = !mfma && !S.noalloc && l->gemm_path == FASTTPS_GEMM_FUSED;
   if (fused && !fused_ok)
     return fail(FASTTPS_ERR_UNSUPPORTED, "the fused kernel is built for one sequence of the Phi-3-mini layer shape");
 
@@ -610,7 +667,8 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint16_t* xb = static_cast<const uint16_t*>(x);
   KernelEvents ev[FASTTPS_NUM_KERNELS];
-  const bool timed = l->prof_n < l->prof_cap;
+  const bool timed = !S.noalloc && l->prof_n < l->prof_cap;
+  const bool debug = !S.noalloc && l->debug;
   if (timed) {
     for (int k = 0; k < FASTTPS_NUM_KERNELS; ++k) {
       const size_t i = ((size_t)l->prof_n * FASTTPS_NUM_KERNELS + k) * 2;
@@ -630,16 +688,17 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   qa.batch = batch;
   qa.x_bf16 = xb;
   qa.gamma = w->attn_norm;
-  qa.out = l->qkv;
+  qa.out = S.qkv;
   qa.eps = c.rms_eps;
+  qa.dbg_act = debug ? l->dbg_h : nullptr;
   GemvArgs oa{};
   oa.w = w->w_o;
   oa.rows = (int)D;
   oa.din = c.n_heads * (int)d;
   oa.batch = batch;
   oa.x_bf16 = xb;
-  oa.in_f32 = l->attn_o;
-  oa.out = l->h1;
+  oa.in_f32 = S.o;
+  oa.out = S.h1;
   oa.eps = c.rms_eps;
   GemvArgs ga{};
   ga.w = w->w_gu;
@@ -647,27 +706,28 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   ga.din = (int)D;
   ga.batch = batch;
   ga.gamma = w->mlp_norm;
-  ga.in_f32 = l->h1;
-  ga.out = l->mlp_a;
+  ga.in_f32 = S.h1;
+  ga.out = S.a;
   ga.eps = c.rms_eps;
+  ga.dbg_act = debug ? l->dbg_h2 : nullptr;
   GemvArgs da{};
   da.w = w->w_down;
   da.rows = (int)D;
   da.din = c.intermediate;
   da.batch = batch;
-  da.in_f32 = l->mlp_a;
-  da.res_f32 = l->h1;
+  da.in_f32 = S.a;
+  da.res_f32 = S.h1;
   da.out_bf16 = static_cast<uint16_t*>(y);
   da.eps = c.rms_eps;
 
   AttnArgs aa{};
-  aa.qkv = l->qkv;
+  aa.qkv = S.qkv;
   aa.rope_cos = l->rope_cos;
   aa.rope_sin = l->rope_sin;
   aa.k_cache = static_cast<uint16_t*>(k_cache);
   aa.v_cache = static_cast<uint16_t*>(v_cache);
-  aa.part = l->attn_part;
-  aa.o = l->attn_o;
+  aa.part = S.part;
+  aa.o = S.o;
   aa.o_operand = mfma ? l->op_o : nullptr;
   aa.o_nbtc = l->nbtc;
   aa.batch = batch;
@@ -676,15 +736,17 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   aa.head_dim = (int)d;
   aa.max_seq = c.max_seq;
   aa.nsplit = nsplit;
-  aa.nsplit_cap = l->nsplit_cap;
+  aa.nsplit_cap = S.nsplit_cap;
   aa.scale = (float)(1.0 / std::sqrt((double)d));
   aa.p_bf16 = l->p_bf16;
   aa.kv_format = kvf;
+  aa.dbg_qk = debug ? l->dbg_qk : nullptr;
   for (int b = 0; b < batch; ++b) aa.pos.p[b] = pos[b];
   // the longest sequences' blocks first (ties in batch order)
   for (int b = 0; b < batch; ++b) aa.order.p[b] = b;
   std::stable_sort(aa.order.p, aa.order.p + batch, [&](int32_t u, int32_t v) { return pos[u] > pos[v]; });
 
+  if (!S.noalloc) l->dbg_written = 0;
   if (fused) {
     FusedArgs f{};
     f.qkv = qa;
@@ -692,6 +754,9 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     f.gateup = ga;
     f.down = da;
     f.attn = aa;
+    // the one-kernel step has no test-hook outputs
+    f.qkv.dbg_act = f.gateup.dbg_act = nullptr;
+    f.attn.dbg_qk = nullptr;
     f.flags = l->fused_flags;
     f.epoch = l->fused_epoch;
     f.err = l->fused_err;
@@ -724,7 +789,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     MfmaArgs m = mfma_args(lt.qkv, w->t_qkv, qa.rows, (int)D);
     m.x_bf16 = xb;
     m.gamma = w->attn_norm;
-    m.out = l->qkv;
+    m.out = S.qkv;
     if ((e = launch_mfma_qkv(m, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
   } else {
     if ((e = launch_rmsnorm_qkv(qa, s, ev[0])) != hipSuccess) return hip_fail(e, "qkv launch");
@@ -742,7 +807,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     m.x_bf16 = xb;
     m.gamma = w->mlp_norm;
     m.a_in = l->op_o;
-    m.out = l->h1;
+    m.out = S.h1;
     m.a_out = l->op_gu;
     m.ssq_out = l->ssq_h1;
     if ((e = launch_mfma_oproj(m, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
@@ -750,12 +815,12 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     m.a_in = l->op_gu;
     m.ssq_in = l->ssq_h1;
     m.ns_in = lt.o.ns;
-    m.out = l->mlp_a;
+    m.out = S.a;
     m.a_out = l->op_down;
     if ((e = launch_mfma_gate_up(m, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
     m = mfma_args(lt.down, w->t_down, (int)D, c.intermediate);
     m.a_in = l->op_down;
-    m.res_f32 = l->h1;
+    m.res_f32 = S.h1;
     m.out_bf16 = static_cast<uint16_t*>(y);
     if ((e = launch_mfma_down(m, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
   } else {
@@ -767,6 +832,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   used(4);
   used(5);
   if (timed) ++l->prof_n;
+  if (debug) l->dbg_written = kDbgQk | (mfma ? 0 : kDbgNorm);
   return FASTTPS_OK;
 }
 
@@ -821,6 +887,18 @@ int fasttps_debug_read(fasttps_layer* l, int32_t which, int32_t batch, void* dst
     case FASTTPS_DBG_H1: src = l->h1; n = (size_t)c.hidden; break;
     case FASTTPS_DBG_MLP_A: src = l->mlp_a; n = (size_t)c.intermediate; break;
     case FASTTPS_DBG_FUSED_WAITS: src = l->fused_err; n = 1; batch = 1; break;
+    case FASTTPS_DBG_QK_ROPE:
+    case FASTTPS_DBG_H:
+    case FASTTPS_DBG_H2: {
+      const int need = which == FASTTPS_DBG_QK_ROPE ? kDbgQk : kDbgNorm;
+      if (!(l->dbg_written & need))
+        return fail(FASTTPS_ERR_INVALID_ARG,
+                    "debug buffer %d was not written by the last step (fasttps_set_debug off, the one-kernel "
+                    "step, or for the normalized activations a matrix-core step)", which);
+      src = which == FASTTPS_DBG_QK_ROPE ? l->dbg_qk : which == FASTTPS_DBG_H ? l->dbg_h : l->dbg_h2;
+      n = which == FASTTPS_DBG_QK_ROPE ? (size_t)(c.n_heads + c.n_kv_heads) * c.head_dim : (size_t)c.hidden;
+      break;
+    }
     default: return fail(FASTTPS_ERR_INVALID_ARG, "unknown debug buffer %d", which);
   }
   n *= (size_t)batch * sizeof(float);
@@ -925,6 +1003,13 @@ int fasttps_set_gemm_path(fasttps_layer* l, int32_t path) {
   if (path == FASTTPS_GEMM_MATRIX && !l->op_o)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer with max_batch > 1");
   l->gemm_path = path;
+  return FASTTPS_OK;
+}
+
+int fasttps_set_debug(fasttps_layer* l, int32_t enable) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  l->debug = enable ? 1 : 0;
   return FASTTPS_OK;
 }
 

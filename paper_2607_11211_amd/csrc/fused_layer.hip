@@ -287,14 +287,15 @@ hipError_t launch_config(const FusedArgs& f, hipStream_t s, KernelEvents ev) {
 bool fused_layer_supported(const FusedShape& sh) {
   // the instantiated shape: the Phi-3-mini layer (d 96, MHA; projections of
   // 3072 inputs with 3 chunks per lane in 2 segments, the down projection's
-  // 8192 inputs with 2 chunks in 8 segments)
+  // 8192 inputs with 2 chunks in 8 segments), each with the ring depth of the
+  // separate GEMV kernel
   return sh.head_dim == 96 && sh.group == 1 && sh.q == FusedShape::Gemv{3, 2, 1} && sh.o == FusedShape::Gemv{3, 2, 1} &&
-         sh.gu == FusedShape::Gemv{3, 2, 1} && sh.down == FusedShape::Gemv{2, 8, 2};
+         sh.gu == FusedShape::Gemv{3, 2, 1} && sh.down == FusedShape::Gemv{2, 8, 1};
 }
 
 hipError_t launch_fused_layer(const FusedArgs& f, const FusedShape& sh, hipStream_t s, KernelEvents ev) {
   if (!fused_layer_supported(sh)) return hipErrorInvalidValue;
-  return launch_config<96, 1, 3, 2, 1, 3, 2, 1, 3, 2, 1, 2, 8, 2>(f, s, ev);
+  return launch_config<96, 1, 3, 2, 1, 3, 2, 1, 3, 2, 1, 2, 8, 1>(f, s, ev);
 }
 
 }  // namespace fasttps

@@ -57,15 +57,12 @@ __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
 }
 
 // Launch shape: a batch tile of BT sequences, MAXCH chunks per lane and row
-// segment, NSEG_H segments per half row, NBUF rows in flight per wave (2-3
-// KB at one sequence, 2-4 KB for batch tiles: at this size the memory
-// system's queues stay short enough that the waves that start last do not
-// finish much later than the rest; the Phi-3 down projection's 2 KB segments
-// one at a time instead of two gave 61.1 -> 60.8 us per layer step, and two
-// or three of the O projection's 3 KB segments instead of one were slower).
+// segment, NSEG_H segments per half row, gemv::ring_rows rows in flight per
+// wave (2-4 KB: at this size the memory system's queues stay short enough
+// that the waves that start last do not finish much later than the rest).
 template <int BT, int MAXCH, int NSEG_H, Mode MODE>
 hipError_t launch_shape(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
-  constexpr int NBUF = (MAXCH >= 3 || (BT == 1 && MAXCH == 2)) ? 1 : 2;
+  constexpr int NBUF = gemv::ring_rows(BT, MAXCH);
   const int nblk = a.rows < kNumCu ? a.rows : kNumCu;
   // unsegmented rows add the residual from the register copy only
   constexpr int NG = kWaves / (halves<MODE>() * NSEG_H);
@@ -133,7 +130,7 @@ FusedShape::Gemv gemv_shape_b1(int din, bool gate_up) {
   const int nseg_h = segments_for(din, cap);
   const int per = (nch + nseg_h * kWave - 1) / (nseg_h * kWave);
   const int maxch = per <= 1 ? 1 : per <= 2 ? 2 : per <= 3 ? 3 : per <= 4 ? 4 : 6;
-  return {maxch, nseg_h, maxch >= 3 ? 1 : 2};
+  return {maxch, nseg_h, gemv::ring_rows(1, maxch)};
 }
 
 hipError_t launch_rmsnorm_qkv(const GemvArgs& a, hipStream_t s, KernelEvents ev) {

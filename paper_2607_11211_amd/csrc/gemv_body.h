@@ -51,7 +51,7 @@ __device__ __forceinline__ void load_slot(v4u (&w)[MAXCH], const v4u* __restrict
   const v4u* row = W + (size_t)(live ? r : rdead) * row_chunks + (live ? hoff : 0);
   const int cmax = live ? nch - 1 : 0;
 #pragma unroll
-  for (int j = 0; j < MAXCH; ++j) w[j] = row[min(cbase + lane + kWave * j, cmax)];
+  for (int j = 0; j < MAXCH; ++j) w[j] = ld_stream(row + min(cbase + lane + kWave * j, cmax));
 }
 
 template <int BT, int MAXCH>
@@ -263,6 +263,22 @@ struct GemvBody {
       }
     }
 
+    // test hook: the normalized activation of this wave's chunks, written by
+    // the first group's waves of the first half (after the stream, so the
+    // ring's waits are not disturbed)
+    if (has_norm<MODE>() && a.dbg_act && grp == 0 && half == 0 && blk == 0) {
+#pragma unroll
+      for (int j = 0; j < MAXCH; ++j) {
+        const int c = cbase + lane + kWave * j;
+        if (c < nch)
+#pragma unroll
+          for (int b = 0; b < BT; ++b)
+            if (b < nb)
+#pragma unroll
+              for (int e = 0; e < 8; ++e) a.dbg_act[(size_t)(b0 + b) * a.din + (size_t)c * 8 + e] = act[b][j][e];
+      }
+    }
+
     // ---- 5. rows cut into segments: add the segments (and siLu_Mul) -------
     if (NSEG > 1) {
       __syncthreads();
@@ -292,6 +308,14 @@ struct GemvBody {
 struct Shape {
   int bt, maxch, nseg_h, nbuf;
 };
+
+// Rows in flight per wave (the ring depth) for a batch tile of bt sequences
+// and maxch chunks per lane: one row of 2 KB or more at one sequence and of
+// 3 KB or more otherwise, else two (2-4 KB in flight per wave). At one
+// sequence the Phi-3 down projection's 2 KB segments one at a time instead of
+// two gave 61.1 -> 60.8 us per layer step on MI355X; two or three of the O
+// projection's 3 KB segments instead of one were slower.
+constexpr int ring_rows(int bt, int maxch) { return (maxch >= 3 || (bt == 1 && maxch == 2)) ? 1 : 2; }
 
 // Chunks per lane allowed for a batch tile: 3 (a lane's activation and ring
 // stay small), or 6 for a single sequence whose rows would otherwise need

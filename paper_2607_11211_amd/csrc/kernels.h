@@ -42,6 +42,8 @@ struct GemvArgs {
   uint16_t* out_bf16;      // down: y [batch, rows] bf16
   float eps;
   int ld;                  // elements per stored row of w (0: din, or 2 din for gate/up)
+  float* dbg_act;          // test hook, null in normal steps: QKV and gate/up write the
+                           // normalized activation (RMSNorm1(x) resp. RMSNorm2(h1)) [batch, din]
 };
 
 // RMSNorm1(x) followed by the fused QKV projection (fp32 out, before RoPE).
@@ -106,6 +108,8 @@ struct AttnArgs {
   int kv_format;           // kKvBf16, kKvFp8 or kKvInt8
   PosArray pos;
   PosArray order;          // grid z -> sequence: the longest first, so the shortest blocks go last
+  float* dbg_qk;           // test hook, null in normal steps: q and k after RoPE (fp32)
+                           // [batch, (H + H_kv) d], q heads first
 };
 // cache element formats (the values of the ABI's FASTTPS_KV_* constants)
 constexpr int kKvBf16 = 0, kKvFp8 = 1, kKvInt8 = 2;

@@ -204,7 +204,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     const int si = min(j / ntp, nstr - 1);
     const int t = min(tbase + j % ntp, a.kt - 1);
     const int s = blk + si * G;
-    wr[r] = W[(((size_t)s * a.kt + t) * 4 + kg) * R + min(n16, R - 1)];
+    wr[r] = ld_stream(W + (((size_t)s * a.kt + t) * 4 + kg) * R + min(n16, R - 1));
     if constexpr (!CACHED) {
       if (MODE == MMode::kQkv) {
 #pragma unroll

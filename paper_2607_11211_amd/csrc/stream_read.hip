@@ -1,5 +1,6 @@
-// Streaming read of device memory with 16-byte loads: the measured HBM read
-// rate next to which the layer's kernels are reported.
+// Streaming read of device memory with 16-byte loads, plain or with the
+// non-temporal cache policy: the measured HBM read rates next to which the
+// layer's kernels are reported.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -10,7 +11,7 @@ namespace {
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
 
-template <int U>
+template <int U, bool NT>
 __global__ __launch_bounds__(kThreads) void stream_read_kernel(const v4u* __restrict__ p, size_t n, unsigned* sink) {
   unsigned acc = 0;
   const size_t stride = (size_t)gridDim.x * kThreads * U;
@@ -19,7 +20,10 @@ __global__ __launch_bounds__(kThreads) void stream_read_kernel(const v4u* __rest
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const size_t j = i + (size_t)u * kThreads;
-      v[u] = j < n ? p[j] : v4u{0, 0, 0, 0};
+      if constexpr (NT)
+        v[u] = j < n ? __builtin_nontemporal_load(p + j) : v4u{0, 0, 0, 0};
+      else
+        v[u] = j < n ? p[j] : v4u{0, 0, 0, 0};
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
@@ -28,20 +32,25 @@ __global__ __launch_bounds__(kThreads) void stream_read_kernel(const v4u* __rest
 }
 
 template <int U>
-hipError_t launch(const void* src, size_t n, unsigned* sink, int blocks, hipStream_t s) {
-  hipLaunchKernelGGL(stream_read_kernel<U>, dim3(blocks), dim3(kThreads), 0, s, static_cast<const v4u*>(src), n,
-                     sink);
+hipError_t launch(const void* src, size_t n, unsigned* sink, int blocks, bool nt, hipStream_t s) {
+  if (nt)
+    hipLaunchKernelGGL((stream_read_kernel<U, true>), dim3(blocks), dim3(kThreads), 0, s,
+                       static_cast<const v4u*>(src), n, sink);
+  else
+    hipLaunchKernelGGL((stream_read_kernel<U, false>), dim3(blocks), dim3(kThreads), 0, s,
+                       static_cast<const v4u*>(src), n, sink);
   return hipGetLastError();
 }
 
 }  // namespace
 
 extern "C" int fasttps_probe_stream_read(const void* src, size_t bytes, void* sink, int blocks, int unroll,
-                                         void* stream, float* ms) {
+                                         int nontemporal, void* stream, float* ms) {
   if (!src || !sink || !ms || bytes == 0 || bytes % 16 || reinterpret_cast<uintptr_t>(src) % 16 ||
       reinterpret_cast<uintptr_t>(sink) % 4 || blocks < 1 || blocks > 65536 ||
-      !(unroll == 1 || unroll == 2 || unroll == 4 || unroll == 8))
+      !(unroll == 1 || unroll == 2 || unroll == 4 || unroll == 8) || (nontemporal != 0 && nontemporal != 1))
     return -1;
+  const bool nt = nontemporal == 1;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (hipEventCreate(&e0) != hipSuccess) return -6;
@@ -54,10 +63,10 @@ extern "C" int fasttps_probe_stream_read(const void* src, size_t bytes, void* si
   hipError_t err = hipEventRecord(e0, s);
   if (err == hipSuccess) {
     switch (unroll) {
-      case 1: err = launch<1>(src, n, k, blocks, s); break;
-      case 2: err = launch<2>(src, n, k, blocks, s); break;
-      case 4: err = launch<4>(src, n, k, blocks, s); break;
-      default: err = launch<8>(src, n, k, blocks, s); break;
+      case 1: err = launch<1>(src, n, k, blocks, nt, s); break;
+      case 2: err = launch<2>(src, n, k, blocks, nt, s); break;
+      case 4: err = launch<4>(src, n, k, blocks, nt, s); break;
+      default: err = launch<8>(src, n, k, blocks, nt, s); break;
     }
   }
   if (err == hipSuccess) err = hipEventRecord(e1, s);

@@ -26,6 +26,7 @@ ERR_HIP = -6
 ERR_BAD_HANDLE = -7
 
 DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A, DBG_FUSED_WAITS = 0, 1, 2, 3, 4
+DBG_QK_ROPE, DBG_H, DBG_H2 = 5, 6, 7
 
 GEMM_AUTO, GEMM_VECTOR, GEMM_MATRIX, GEMM_FUSED = 0, 1, 2, 3
 
@@ -36,7 +37,8 @@ KV_FORMATS = {"fp8_e4m3": KV_FP8_E4M3, "int8": KV_INT8}
 EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
-           "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
+           "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_set_debug", "fasttps_validate_step",
+           "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 7
 
 
@@ -73,6 +75,8 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_unfused_enable.argtypes = [vp]
     lib.fasttps_set_attention_p_bf16.argtypes = [vp, i32]
     lib.fasttps_set_gemm_path.argtypes = [vp, i32]
+    lib.fasttps_set_debug.argtypes = [vp, i32]
+    lib.fasttps_validate_step.argtypes = [ctypes.POINTER(Config), vp, ctypes.POINTER(i32), i32, vp, vp, vp, i32]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
     lib.fasttps_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
@@ -87,7 +91,8 @@ def _load() -> ctypes.CDLL:
     for name in ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step", "fasttps_debug_read",
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
                  "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
-                 "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8", "fasttps_set_gemm_path"):
+                 "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8", "fasttps_set_gemm_path",
+                 "fasttps_set_debug", "fasttps_validate_step"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -113,6 +118,17 @@ def make_config(cfg, max_batch: Optional[int] = None) -> Config:
     return Config(cfg.hidden, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.intermediate,
                   cfg.batch if max_batch is None else max_batch, cfg.max_seq, float(cfg.rope_base),
                   float(cfg.rms_eps))
+
+
+def validate_step(cfg, x_addr: int, pos, k_addr: int, v_addr: int, y_addr: int, cache_elem_bytes: int = 2,
+                  max_batch: Optional[int] = None) -> int:
+    """Status of a step's argument checks against a layer config (host only:
+    addresses are examined, never dereferenced; no GPU needed)."""
+    c = make_config(cfg, max_batch)
+    p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
+    return int(LIB.fasttps_validate_step(ctypes.byref(c), x_addr or None,
+                                         p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(p.shape[0]),
+                                         k_addr or None, v_addr or None, y_addr or None, int(cache_elem_bytes)))
 
 
 def _ptr(t) -> int:
@@ -218,6 +234,10 @@ class Layer:
                "fasttps_debug_read")
         torch.cuda.synchronize()
         return int(t.item())
+
+    def set_debug(self, enable: bool) -> None:
+        """Test hook: later steps also write q, k after RoPE and the two normalized activations."""
+        _check(LIB.fasttps_set_debug(self.handle, 1 if enable else 0), "fasttps_set_debug")
 
     def set_attention_p_bf16(self, enable: bool) -> None:
         """Accuracy study only: round the softmax weights to bf16 before PV."""

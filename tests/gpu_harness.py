@@ -2,11 +2,11 @@
 compare it with the fp64 oracle on the same seeded inputs.
 
 The appended K/V are held to one bf16 ulp of the oracle's exact values
-(reading R16); where the GPU's rounding of an entry lands on the other
-neighbour, the attention and everything after it are compared with the
-oracle run on the GPU's stored entries (reading R9: attention reads the
-stored entry), so that one legitimate rounding is not charged to the
-attention's 1e-4 bar."""
+(reading R16), and y to 2e-2 max(1, |ref|) of the oracle on the same seeded
+inputs. Where the GPU's rounding of an entry lands on the other neighbour,
+the intermediates after it (o, h1, a) are compared with the oracle run on
+the GPU's stored entries (reading R9: attention reads the stored entry), so
+that one legitimate rounding is not charged to the attention's 1e-4 bar."""
 from __future__ import annotations
 
 import sys
@@ -52,6 +52,8 @@ def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=
     lay = layer if layer is not None else L.Layer(cfg, max_batch=max_batch)
     if gemm_path is not None:
         lay.set_gemm_path(gemm_path)
+    if debug and not unfused:
+        lay.set_debug(True)
     W = weights
     if W is None:
         wt = {k: L.to_device(v) for k, v in inp.weights.items()}
@@ -78,11 +80,21 @@ def run_gpu(cfg, inp, layer=None, weights=None, debug=True, keep=False, unfused=
     if debug:
         dev = x.device
         bufs = {"qkv": (L.DBG_QKV, cfg.qkv_rows), "o": (L.DBG_ATTN, cfg.q_dim), "h1": (L.DBG_H1, cfg.hidden),
-                "a": (L.DBG_MLP_A, cfg.intermediate)}
+                "a": (L.DBG_MLP_A, cfg.intermediate), "qk_rope": (L.DBG_QK_ROPE, cfg.q_dim + cfg.kv_dim),
+                "h": (L.DBG_H, cfg.hidden), "h2": (L.DBG_H2, cfg.hidden)}
         for name, (which, n) in bufs.items():
             t = torch.empty(B, n, dtype=torch.float32, device=dev)
-            lay.debug_read(which, B, t)
+            try:
+                lay.debug_read(which, B, t)
+            except L.FastTPSError as ex:
+                # the one-kernel step writes none of the test-hook outputs, the
+                # matrix-core path not the normalized activations
+                optional = ("h", "h2") if gemm_path != L.GEMM_FUSED else ("qk_rope", "h", "h2")
+                if name in optional and ex.status == L.ERR_INVALID_ARG:
+                    continue
+                raise
             out[name] = t
+        lay.set_debug(False)
     torch.cuda.synchronize()
     if kv8 is not None:
         res = {"y": L.from_device(y), "k_cache": kc.cpu().numpy(), "v_cache": vc.cpu().numpy()}
@@ -141,6 +153,18 @@ def check_intermediates(cfg, inp, gpu, r):
     e = np.abs(gpu["qkv"] - qkv_ref) / np.max(np.abs(qkv_ref), axis=1, keepdims=True)
     worst["qkv"] = float(e.max())
     assert e.max() <= QKV_TOL, f"qkv: {e.max():.3g}"
+    # q and k after the joint RoPE, before k is rounded for the cache
+    if "qk_rope" in gpu:
+        qk_ref = np.concatenate([r["q_rope"].reshape(B, -1), r["k_rope"].reshape(B, -1)], axis=1)
+        e = np.abs(gpu["qk_rope"] - qk_ref) / np.max(np.abs(qk_ref), axis=1, keepdims=True)
+        worst["qk_rope"] = float(e.max())
+        assert e.max() <= QKV_TOL, f"q, k after RoPE: {e.max():.3g}"
+    # the normalized activations (vector path)
+    for name in ("h", "h2"):
+        if name in gpu:
+            e = np.abs(gpu[name] - r[name]) / np.max(np.abs(r[name]), axis=1, keepdims=True)
+            worst[name] = float(e.max())
+            assert e.max() <= QKV_TOL, f"{name}: {e.max():.3g}"
     o = gpu["o"].reshape(B, H, d)
     e = np.abs(o - r["o"]) / np.max(np.abs(r["o"]), axis=2, keepdims=True)
     worst["o"] = float(e.max())
@@ -166,17 +190,24 @@ def appended_entries(cfg, inp, gpu):
 
 def full_check(cfg, inp, gpu, r, intermediates=True):
     """The cache against the oracle (untouched bytes exact, appended entries
-    within one ulp); y and the intermediates against the oracle run on the
-    GPU's own appended entries where those differ from the oracle's (the
-    attention reads the stored, rounded entry; a one-ulp rounding of it
-    would otherwise be charged to the attention and everything after it)."""
+    within one ulp) and y against the oracle on the same seeded inputs
+    (2e-2 max(1, |ref|) per element), always. The intermediates (o, h1, a)
+    are compared with the oracle run on the GPU's own appended entries where
+    those differ from the oracle's (the attention reads the stored, rounded
+    entry; a one-ulp rounding of it would otherwise be charged to the
+    attention's 1e-4 bar); y is then also logged against that oracle."""
     stats = check_cache(cfg, inp, gpu, r)
-    gk, gv = appended_entries(cfg, inp, gpu)
-    if not (np.array_equal(gk, r["k_new_bits"]) and np.array_equal(gv, r["v_new_bits"])):
-        r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights, new_entries=(gk, gv))
-        stats["teacher_forced"] = True
     yerr = check_y(gpu, r)
-    worst = check_intermediates(cfg, inp, gpu, r) if intermediates else {}
-    log(f"{cfg.name}: pos={inp.pos.tolist()[:8]} y_err={yerr:.2e} cache={stats} inter={worst}")
+    gk, gv = appended_entries(cfg, inp, gpu)
+    r_int = r
+    yerr_tf = None
+    if not (np.array_equal(gk, r["k_new_bits"]) and np.array_equal(gv, r["v_new_bits"])):
+        r_int = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights,
+                                     new_entries=(gk, gv))
+        stats["stored_entries_differ"] = True
+        yerr_tf = check_y(gpu, r_int)
+    worst = check_intermediates(cfg, inp, gpu, r_int) if intermediates else {}
+    log(f"{cfg.name}: pos={inp.pos.tolist()[:8]} y_err={yerr:.2e}"
+        + (f" (vs the oracle on the GPU's stored entries {yerr_tf:.2e})" if yerr_tf is not None else "")
+        + f" cache={stats} inter={worst}")
     return stats, yerr, worst
-

@@ -94,12 +94,17 @@ def run_case(cfg, inp, fmt, layer=None, weights=None):
     gv = np.stack([gpu["v_cache"][b, :, int(inp.pos[b]), :] for b in range(B)])
     mk = check_codes(cfg, inp, fmt, kc, gpu["k_cache"], r["k_rope"], ks, r["k_new_bits"], "k")
     mv = check_codes(cfg, inp, fmt, vc, gpu["v_cache"], r["v"], vs, r["v_new_bits"], "v")
+    # y against the oracle on the same seeded inputs, always; the intermediates
+    # against the oracle run on the GPU's stored codes where a code landed on
+    # the other side of a rounding boundary (the attention reads the stored code)
+    yerr = check_y(gpu, r)
     r_tf = r if (mk == 0 and mv == 0) else ref.decode_layer_cfg(cfg, inp.x, inp.pos, kc, vc, W, kv=kv,
                                                                 new_entries=(gk, gv))
-    yerr = check_y(gpu, r_tf)
+    yerr_tf = check_y(gpu, r_tf) if r_tf is not r else None
     worst = check_intermediates(cfg, inp, gpu, r_tf)
     log(f"{cfg.name} {fmt}: pos={inp.pos.tolist()[:8]} code mismatches k {mk} v {mv} of {B * G * cfg.head_dim} "
-        f"each; y_err={yerr:.2e} inter={worst}")
+        f"each; y_err={yerr:.2e}" + (f" (vs the oracle on the stored codes {yerr_tf:.2e})" if yerr_tf is not None
+                                     else "") + f" inter={worst}")
     return gpu, r_tf
 
 
@@ -153,6 +158,9 @@ def test_kv8_consecutive_steps(fmt):
                                           v_cache=host_v)
             check_codes(cfg, step_inp, fmt, host_k, gk, r["k_rope"], ks, r["k_new_bits"], "k")
             check_codes(cfg, step_inp, fmt, host_v, gv, r["v"], vs, r["v_new_bits"], "v")
+            # y against the oracle on this step's inputs (the caches as the
+            # GPU left them after the previous steps), then on its stored codes
+            check_y({"y": L.from_device(y)}, r)
             r = ref.decode_layer_cfg(cfg, x_bits, pos, host_k, host_v, W, kv=kv, new_entries=(sk, sv))
             check_y({"y": L.from_device(y)}, r)
             host_k, host_v = gk, gv
