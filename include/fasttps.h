@@ -128,6 +128,24 @@ FASTTPS_API int fasttps_decode_step(fasttps_layer* layer, const fasttps_weights*
                         const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
                         void* y, void* stream);
 
+/* fasttps_decode_step for callers that cannot allocate (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, checks, cache contract and results, computed by the same
+ * vector-path kernels (whatever fasttps_set_gemm_path says), with the step's
+ * fp32 intermediates in a static device array of the library (8 MiB per
+ * device, held until the process ends) instead of the handle's scratch. The
+ * call allocates nothing. Returns FASTTPS_ERR_UNSUPPORTED, before any
+ * launch, when the step's intermediates (q|k|v, the attention's split
+ * partials, o, h1 and the MLP activation, each 256-byte aligned, for `batch`
+ * sequences) exceed 8 MiB; the five workloads of this library need at most
+ * about 3 MiB (16 sequences of the Phi-3-mini layer). Every call on a device
+ * shares that device's array and overwrites it, so calls on one device
+ * whose executions overlap (different streams, or threads) race; the test
+ * hooks (fasttps_debug_read, fasttps_profile_*) do not see these steps. */
+FASTTPS_API int fasttps_decode_step_noalloc(fasttps_layer* layer, const fasttps_weights* w, const void* x,
+                                            const int32_t* pos, int32_t batch, void* k_cache, void* v_cache,
+                                            void* y, void* stream);
+
 /* 8-bit KV cache formats for fasttps_decode_step_kv8. */
 #define FASTTPS_KV_FP8_E4M3 1 /* OCP E4M3: bias 7, subnormals, largest finite 448, 0x7F/0xFF NaN */
 #define FASTTPS_KV_INT8 2     /* two's complement, entries in [-127, 127] */

@@ -113,8 +113,41 @@ constexpr int kInterlaceTile = 1;
 // test-hook buffers a step wrote (fasttps_layer::dbg_written)
 constexpr int kDbgQk = 1, kDbgNorm = 2;
 
+// The allocation-free step's scratch (fasttps_decode_step_noalloc): one
+// statically sized array per device, reached through the address
+// hipGetSymbolAddress gives for each device (the array's name in host code
+// is a stand-in, not a device address). Looked up once per device by
+// fasttps_layer_create, with that device current.
+constexpr size_t kStaticScratchBytes = size_t(8) << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
 }  // namespace
 
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+
+// The device address of this device's static scratch array (dev current).
+hipError_t static_scratch_lookup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return hipSuccess;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  g_scratch_ptr[dev] = p;
+  return hipSuccess;
+}
+
+void* static_scratch(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
 
 struct fasttps_layer {
   uint64_t magic;
@@ -323,6 +356,10 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   if (e != hipSuccess) {
     delete l;
     return hip_fail(e, "hipGetDevice");
+  }
+  if ((e = static_scratch_lookup(dev)) != hipSuccess) {
+    delete l;
+    return hip_fail(e, "hipGetSymbolAddress of the static scratch");
   }
   void* arena = nullptr;
   e = hipMalloc(&arena, total);
@@ -610,8 +647,9 @@ int attention_splits(const fasttps_layer* l, const int32_t* pos, int32_t batch, 
   return ceil_div(maxn, split_len);
 }
 
-// Where a step keeps its fp32 intermediates (by default the layer handle's
-// scratch).
+// Where a step keeps its fp32 intermediates: the layer handle's scratch, or
+// (the allocation-free step) the static array, with the split partials laid
+// out for exactly the step's nsplit splits.
 struct StepScratch {
   float* qkv;
   float* part;
@@ -619,8 +657,29 @@ struct StepScratch {
   float* h1;
   float* a;
   int nsplit_cap;
-  bool noalloc;  // scratch not owned by the handle: the vector path only, no test hooks, no timing events
+  bool noalloc;  // the vector path only, no test hooks, no timing events
 };
+
+// Bytes of static scratch a step of `batch` sequences with nsplit splits
+// needs, and the layout (offsets in floats) if `out` is set.
+size_t noalloc_layout(const fasttps_config& c, int batch, int nsplit, float* base, StepScratch* out) {
+  const size_t B = batch, d = c.head_dim;
+  const size_t sizes[5] = {B * (c.n_heads + 2 * c.n_kv_heads) * d * sizeof(float),
+                           B * c.n_heads * nsplit * (d + 2) * sizeof(float), B * c.n_heads * d * sizeof(float),
+                           B * c.hidden * sizeof(float), B * c.intermediate * sizeof(float)};
+  size_t offs[5], total = 0;
+  for (int i = 0; i < 5; ++i) {
+    offs[i] = total;
+    total += align256(sizes[i]);
+  }
+  if (out) {
+    char* p = reinterpret_cast<char*>(base);
+    *out = StepScratch{reinterpret_cast<float*>(p + offs[0]), reinterpret_cast<float*>(p + offs[1]),
+                       reinterpret_cast<float*>(p + offs[2]), reinterpret_cast<float*>(p + offs[3]),
+                       reinterpret_cast<float*>(p + offs[4]), nsplit, true};
+  }
+  return total;
+}
 
 // The fused step after validation: kvf is the cache format (kKvBf16, or an
 // 8-bit format with its scales in *sc); scr overrides the layer's scratch.
@@ -847,6 +906,25 @@ int fasttps_decode_step(fasttps_layer* l, const fasttps_weights* w, const void* 
   const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
   if (st) return st;
   return run_step(l, w, x, pos, batch, k_cache, v_cache, y, stream, maxp, kKvBf16, nullptr);
+}
+
+int fasttps_decode_step_noalloc(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,
+                                int32_t batch, void* k_cache, void* v_cache, void* y, void* stream) {
+  g_last_error.clear();
+  int maxp = 0;
+  const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
+  if (st) return st;
+  const int nsplit = attention_splits(l, pos, batch, maxp);
+  const size_t need = noalloc_layout(l->cfg, batch, nsplit, nullptr, nullptr);
+  if (need > kStaticScratchBytes)
+    return fail(FASTTPS_ERR_UNSUPPORTED,
+                "the allocation-free step needs %zu bytes of scratch for %d sequences; its static buffer holds %zu",
+                need, batch, kStaticScratchBytes);
+  float* base = static_cast<float*>(static_scratch(l->device));
+  if (!base) return fail(FASTTPS_ERR_HIP, "no static scratch address for device %d", l->device);
+  StepScratch scr{};
+  noalloc_layout(l->cfg, batch, nsplit, base, &scr);
+  return run_step(l, w, x, pos, batch, k_cache, v_cache, y, stream, maxp, kKvBf16, nullptr, &scr);
 }
 
 int fasttps_decode_step_kv8(fasttps_layer* l, const fasttps_weights* w, const void* x, const int32_t* pos,

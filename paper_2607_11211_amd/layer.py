@@ -38,6 +38,7 @@ EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step"
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
            "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_set_debug", "fasttps_validate_step",
+           "fasttps_decode_step_noalloc",
            "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 7
 
@@ -70,6 +71,7 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_weights_pack.argtypes = [vp, ctypes.POINTER(WeightsDesc), vp, ctypes.POINTER(vp)]
     lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     lib.fasttps_decode_step_unfused.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
+    lib.fasttps_decode_step_noalloc.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
     fp = ctypes.POINTER(ctypes.c_float)
     lib.fasttps_decode_step_kv8.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, i32, vp, vp, fp, fp, vp, vp]
     lib.fasttps_unfused_enable.argtypes = [vp]
@@ -92,7 +94,7 @@ def _load() -> ctypes.CDLL:
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
                  "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
                  "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8", "fasttps_set_gemm_path",
-                 "fasttps_set_debug", "fasttps_validate_step"):
+                 "fasttps_set_debug", "fasttps_validate_step", "fasttps_decode_step_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -185,6 +187,15 @@ class Layer:
                                        p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
                                        _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step")
+
+    def step_noalloc(self, weights: Weights, x, pos, k_cache, v_cache, y, stream=None) -> None:
+        """Enqueue one decode step that allocates nothing (the library's static
+        scratch array; vector-path kernels). Same contract as step."""
+        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
+        _check(LIB.fasttps_decode_step_noalloc(self.handle, weights.handle, _ptr(x),
+                                               p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(p.shape[0]),
+                                               _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
+               "fasttps_decode_step_noalloc")
 
     def step_kv8(self, weights: Weights, fmt: str, x, pos, k_cache, v_cache, k_scale, v_scale, y,
                  stream=None) -> None:
