@@ -55,29 +55,39 @@ using attn::kThreads;
 using attn::merge_factor;
 
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head); one combine thread each
+// bf16 caches: whole-line non-temporal loads and the LDS exchange (AttnBody
+// XCH) for one or two query heads per KV head and splits of at least
+// kXchMinTiles tiles. Measured on MI355X (per layer step, HIP graph): the
+// 16-sequence ragged Phi-3 batch (splits of 9 tiles) attention 88.3 -> 77.0
+// us; Phi-3 at KV 4096 (4 tiles) 11.45 -> 11.42; at KV 1024 (1 tile) 5.65 ->
+// 7.28; the GQA layer (groups of four, one tile in flight per lane at 256
+// VGPRs) 105.8 -> 124.3.
+constexpr int kXchMinTiles = 8;
 
 // one (split, KV head, sequence) per block
-template <int D, int G, int NRING, bool PBF16, int KVF>
+template <int D, int G, int NRING, bool PBF16, int KVF, bool XCH>
 __device__ __forceinline__ void attn_split_body(const AttnArgs& a, float kscale, float vscale) {
+  using Body = attn::AttnBody<D, G, NRING, PBF16, KVF, attn::GlobalIO, XCH>;
   __shared__ attn::AttnSmem<D, G, KVF> sm;
-  attn::AttnBody<D, G, NRING, PBF16, KVF, attn::GlobalIO> body(a, attn::GlobalIO{}, sm, threadIdx.x, blockIdx.x,
-                                                               blockIdx.y, a.order.p[blockIdx.z], true);
+  __shared__ v4u xch[XCH ? 2 * (kThreads / kWave) * Body::SPAN : 1];  // K spans, then V spans
+  Body body(a, attn::GlobalIO{}, sm, threadIdx.x, blockIdx.x, blockIdx.y, a.order.p[blockIdx.z], true, xch,
+            xch + (kThreads / kWave) * Body::SPAN);
   body.load_prologue();
   __builtin_amdgcn_sched_barrier(0);  // keep the prologue loads ahead of the tiles
   body.prime();
   body.run(kscale, vscale);
 }
 
-template <int D, int G, int NRING, bool PBF16>
+template <int D, int G, int NRING, bool PBF16, bool XCH>
 __global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
-  attn_split_body<D, G, NRING, PBF16, kKvBf16>(a, 1.f, 1.f);
+  attn_split_body<D, G, NRING, PBF16, kKvBf16, XCH>(a, 1.f, 1.f);
 }
 
 // 8-bit cache: the KV head's two scales come from the argument block; tiles
 // in flight as for a bf16 cache
 template <int D, int G, int KVF>
 __global__ __launch_bounds__(kThreads) void attn_split_kv8_kernel(AttnArgs a, KvScales sc) {
-  attn_split_body<D, G, (G <= 2 ? 2 : 1), false, KVF>(a, sc.k[blockIdx.y], sc.v[blockIdx.y]);
+  attn_split_body<D, G, (G <= 2 ? 2 : 1), false, KVF, false>(a, sc.k[blockIdx.y], sc.v[blockIdx.y]);
 }
 
 // o[b, h] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s,  M = max_s m_s.
@@ -220,8 +230,15 @@ hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   // per CU the split targets), one for groups of four (up to 256 VGPRs)
   constexpr int NRING = G <= 2 ? 2 : 1;
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
-  if (a.p_bf16) return ext_launch(attn_split_kernel<D, G, NRING, true>, grid, dim3(kThreads), 0, s, ev, a);
-  return ext_launch(attn_split_kernel<D, G, NRING, false>, grid, dim3(kThreads), 0, s, ev, a);
+  int maxp = 0;
+  for (int b = 0; b < a.batch; ++b) maxp = a.pos.p[b] > maxp ? a.pos.p[b] : maxp;
+  const int tiles = (maxp + attn::kTile - 1) / attn::kTile;
+  const bool xch = G <= 2 && (tiles + a.nsplit - 1) / a.nsplit >= kXchMinTiles;
+  if (a.p_bf16)
+    return xch ? ext_launch(attn_split_kernel<D, G, NRING, true, true>, grid, dim3(kThreads), 0, s, ev, a)
+               : ext_launch(attn_split_kernel<D, G, NRING, true, false>, grid, dim3(kThreads), 0, s, ev, a);
+  return xch ? ext_launch(attn_split_kernel<D, G, NRING, false, true>, grid, dim3(kThreads), 0, s, ev, a)
+             : ext_launch(attn_split_kernel<D, G, NRING, false, false>, grid, dim3(kThreads), 0, s, ev, a);
 }
 
 template <int D, int G>

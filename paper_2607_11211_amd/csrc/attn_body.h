@@ -156,6 +156,24 @@ __device__ __forceinline__ void tile_load(Chunk (&k)[NC], Chunk (&v)[NC], const 
   }
 }
 
+// The contiguous variant (bf16 cache): a wave's 16 positions of a tile are
+// 16 consecutive rows, one contiguous span of 16 RC16 16-byte chunks; lane l
+// loads chunks l, l + 64, ... of it (each load instruction one contiguous
+// kilobyte, whole 128-byte lines), with the non-temporal policy of the
+// weight streams; rows past `last` are clamped to it. The chunks reach the
+// lanes that compute with them through the wave's LDS exchange area.
+template <int RC16, int NC>
+__device__ __forceinline__ void tile_load_contig(v4u (&k)[NC], v4u (&v)[NC], const v4u* __restrict__ Kc,
+                                                 const v4u* __restrict__ Vc, int t0, int last, int wave, int lane) {
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int q = lane + kWave * c;
+    const size_t at = (size_t)min(t0 + 16 * wave + q / RC16, last) * RC16 + q % RC16;
+    k[c] = ld_stream(Kc + at);
+    v[c] = ld_stream(Vc + at);
+  }
+}
+
 // Plain global-memory IO of the attention kernel.
 struct GlobalIO {
   __device__ __forceinline__ float qkv(const AttnArgs& a, size_t i) const { return a.qkv[i]; }
@@ -169,7 +187,10 @@ struct GlobalIO {
 // of an 8-bit cache (unused for bf16). live = false runs the item's barriers
 // and nothing else (no positions, no stores), for a quarter of a fused block
 // without an item.
-template <int D, int G, int NRING, bool PBF16, int KVF, class IO>
+// XCH: the contiguous loads and the LDS exchange (bf16 caches; xk, xv each
+// hold kThreads / kWave spans of 16 RC rows, one per wave); otherwise each
+// lane loads its quarter rows itself with plain loads.
+template <int D, int G, int NRING, bool PBF16, int KVF, class IO, bool XCH = false>
 struct AttnBody {
   using R = LaneRow<D, KVF>;
   using Chunk = typename R::Chunk;
@@ -177,13 +198,17 @@ struct AttnBody {
   static constexpr int NC = R::NC;    // chunks per lane (K and V each)
   static constexpr int RC = D * kv_bytes<KVF>() / 16;  // 16-byte chunks per row (the append)
   static constexpr int HALF = D / 2;
+  static constexpr int SPAN = 16 * RC;  // chunks of a wave's 16 rows (XCH)
   static_assert(SEG == NC * R::EPC, "a lane's quarter row must be whole chunks");
   static_assert(G * HALF <= kThreads && D <= kThreads, "one prologue element per thread");
+  static_assert(!XCH || (KVF == kKvBf16 && SPAN == kWave * NC), "the exchange covers a wave's rows in NC loads");
   using Smem = AttnSmem<D, G, KVF>;
 
   const AttnArgs& a;
   IO io;
   Smem& sm;
+  v4u* xk;  // XCH: this wave's exchange spans (LDS)
+  v4u* xv;
   int tid, s, g, b, P, start, stride, end, last, j, seg, pj, ph;
   bool own_new, live;
   size_t head_off;
@@ -194,8 +219,10 @@ struct AttnBody {
   Chunk kr[NRING][NC], vr[NRING][NC];
 
   __device__ __forceinline__ AttnBody(const AttnArgs& a_, IO io_, Smem& sm_, int tid_, int s_, int g_, int b_,
-                                      bool live_)
+                                      bool live_, v4u* xk_ = nullptr, v4u* xv_ = nullptr)
       : a(a_), io(io_), sm(sm_), tid(tid_), s(s_), g(g_), b(b_), live(live_) {
+    xk = xk_ + (tid_ / kWave) * SPAN;
+    xv = xv_ + (tid_ / kWave) * SPAN;
     P = a.pos.p[b];
     // tiles s, s + nsplit, ... of the sequence's cached entries [0, P); the
     // new entry P is added from LDS by the split whose tile index holds it
@@ -236,7 +263,41 @@ struct AttnBody {
   // ---- the ring's first NRING tiles ----------------------------------------
   __device__ __forceinline__ void prime() {
 #pragma unroll
-    for (int r = 0; r < NRING; ++r) tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, start + r * stride, last, j, seg);
+    for (int r = 0; r < NRING; ++r) refill(r, start + r * stride);
+  }
+
+  // ring slot r <- the tile at t0
+  __device__ __forceinline__ void refill(int r, int t0) {
+    if constexpr (XCH)
+      tile_load_contig<RC, NC>(kr[r], vr[r], Kc, Vc, t0, last, tid / kWave, tid % kWave);
+    else
+      tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, t0, last, j, seg);
+  }
+
+  // this lane's quarter rows of ring slot r: the slot itself, or (XCH) its
+  // chunks through the wave's exchange spans (wave-private, so no barrier:
+  // a wave's LDS accesses take effect in program order)
+  __device__ __forceinline__ void lane_rows(int r, Chunk (&kq)[NC], Chunk (&vq)[NC]) {
+    if constexpr (XCH) {
+      const int lane = tid % kWave;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        xk[lane + kWave * c] = kr[r][c];
+        xv[lane + kWave * c] = vr[r][c];
+      }
+      const int at = (lane >> 2) * RC + (lane & 3) * NC;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        kq[c] = xk[at + c];
+        vq[c] = xv[at + c];
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        kq[c] = kr[r][c];
+        vq[c] = vr[r][c];
+      }
+    }
   }
 
   __device__ __forceinline__ void run(float kscale, float vscale) {
@@ -315,16 +376,20 @@ struct AttnBody {
       for (int r = 0; r < NRING; ++r) {
         const int tt = t0 + r * stride;
         float kf[SEG], vf[SEG];
+        {
+          Chunk kq[NC], vq[NC];
+          lane_rows(r, kq, vq);
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          decode_chunk<KVF>(kr[r][c], kf + R::EPC * c);
-          decode_chunk<KVF>(vr[r][c], vf + R::EPC * c);
+          for (int c = 0; c < NC; ++c) {
+            decode_chunk<KVF>(kq[c], kf + R::EPC * c);
+            decode_chunk<KVF>(vq[c], vf + R::EPC * c);
+          }
         }
         // refill the slot with the tile NRING further on (clamped past the end);
         // the barrier keeps the refill after the unpack, so the new tile lands
         // in the registers the old one leaves (no copies, no early waits)
         __builtin_amdgcn_sched_barrier(0);
-        tile_load<R::ROW_CHUNKS>(kr[r], vr[r], Kc, Vc, tt + NRING * stride, last, j, seg);
+        refill(r, tt + NRING * stride);
         update(kf, vf, tt + j < end);
       }
     }

@@ -66,6 +66,25 @@ SMALL = [
 ]
 
 
+# splits of 8 tiles and more with one or two query heads per KV head take the
+# attention's contiguous-load variant (whole-line loads, LDS exchange): every
+# head dimension and both group sizes, and a ragged batch
+XCH = [LayerConfig(name=f"x_d{d}_g{g}", index=70 + i, batch=1, hidden=512, n_heads=32 * g, n_kv_heads=32,
+                   head_dim=d, intermediate=512, rope_base=10000.0, max_seq=8256, pos=(8192,))
+       for i, (d, g) in enumerate([(64, 1), (96, 1), (128, 1), (64, 2), (96, 2), (128, 2)])]
+XCH.append(LayerConfig(name="x_d96_ragged3", index=76, batch=3, hidden=512, n_heads=32, n_kv_heads=32, head_dim=96,
+                       intermediate=512, rope_base=10000.0, max_seq=16064, pos=(16000, 9000, 12345)))
+
+
+@pytest.mark.parametrize("cfg", XCH, ids=lambda c: c.name)
+def test_contiguous_attention_shapes(cfg):
+    log(f"start {cfg.name}")
+    inp = inputs.make_layer_inputs(cfg)
+    r = ref.decode_layer_cfg(cfg, inp.x, inp.pos, inp.k_cache, inp.v_cache, inp.weights)
+    gpu = run_gpu(cfg, inp)
+    full_check(cfg, inp, gpu, r)
+
+
 @pytest.mark.parametrize("cfg", SMALL, ids=lambda c: c.name)
 def test_small_shapes(cfg):
     log(f"start {cfg.name}")
