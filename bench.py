@@ -49,9 +49,11 @@ def log(msg: str) -> None:
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_bytes(cfg, pos, kv_elem_bytes: int = 2):
+def kernel_bytes(cfg, pos, kv_elem_bytes: int = 2, mlp_fused: bool = False):
     """Algorithmic HBM bytes per launch of each kernel (weights once, K/V read
-    once; an 8-bit cache reads one byte per element)."""
+    once; an 8-bit cache reads one byte per element). With the fused MLP the
+    slot of the gate/up kernel is the fused kernel (W_gu and W_down) and the
+    slot of the down kernel the partial-sum reduction."""
     D, K, d = cfg.hidden, cfg.intermediate, cfg.head_dim
     kv = cfg.kv_read_bytes(pos) * kv_elem_bytes // 2
     return {
@@ -59,8 +61,8 @@ def kernel_bytes(cfg, pos, kv_elem_bytes: int = 2):
         "attention": kv,
         "attn_combine": 0,
         "oproj_residual": 2 * D * cfg.q_dim,
-        "mlp_gate_up": 2 * 2 * K * D + 2 * D,
-        "mlp_down": 2 * K * D,
+        "mlp_gate_up": 2 * 2 * K * D + 2 * D + (2 * K * D if mlp_fused else 0),
+        "mlp_down": 0 if mlp_fused else 2 * K * D,
         "fused_layer": cfg.weight_bytes() + kv,
     }
 
@@ -337,7 +339,7 @@ def sweep(args) -> int:
     return 0
 
 
-def build_workload(cfg, pos, args, kv: str, gemm: str, log_prefix: str = ""):
+def build_workload(cfg, pos, args, kv: str, gemm: str, log_prefix: str = "", mlp: str = "split"):
     """Resident device copies of a workload: the layers of a stack, or for a
     single layer a chain of independent copies (own weights and caches)
     totalling at least 2 GB (at most 32 copies), so that no copy is still in
@@ -348,7 +350,7 @@ def build_workload(cfg, pos, args, kv: str, gemm: str, log_prefix: str = ""):
     from paper_2607_11211_amd import inputs
     from paper_2607_11211_amd import layer as L
     kv8 = kv != "bf16"
-    kb = kernel_bytes(cfg, pos, 1 if kv8 else 2)
+    kb = kernel_bytes(cfg, pos, 1 if kv8 else 2, mlp_fused=mlp == "fused")
     step_bytes = kb["fused_layer"]
     # (a step of a few MB is latency-bound and cached anyway: 32 copies)
     nl = cfg.layers if cfg.layers > 1 else min(max(1, -(-ROTATE_BYTES // step_bytes)), 32)
@@ -356,6 +358,8 @@ def build_workload(cfg, pos, args, kv: str, gemm: str, log_prefix: str = ""):
     gemm_id = {"auto": L.GEMM_AUTO, "vector": L.GEMM_VECTOR, "matrix": L.GEMM_MATRIX, "fused": L.GEMM_FUSED}[gemm]
     lay = L.Layer(cfg, max_batch=max(cfg.batch, 2) if gemm == "matrix" else None)
     lay.set_gemm_path(gemm_id)
+    if mlp == "fused":
+        lay.set_mlp_path(L.MLP_FUSED)   # before packing: the weights then carry W_down's slices
     weights, kcs, vcs, kss, vss = [], [], [], [], []
     gen = torch.Generator(device="cuda")
     gen.manual_seed(0xFA57 + cfg.index)
@@ -566,6 +570,9 @@ def main() -> int:
     ap.add_argument("--batch", type=int, default=None,
                     help="run the workload with this many sequences instead of its own batch (each at the "
                          "workload's KV length, or drawn from a ragged workload's range)")
+    ap.add_argument("--mlp", choices=["split", "fused"], default="split",
+                    help="MLP kernels: gate/up storing h^sm and a separate down projection (default), or the fused "
+                         "MLP keeping h^sm on chip with a partial-sum reduction")
     ap.add_argument("--kv", choices=["bf16", "fp8_e4m3", "int8"], default="bf16",
                     help="KV cache element format: bf16, or 8-bit codes with one scale per KV head "
                          "(fasttps_decode_step_kv8)")
@@ -605,11 +612,14 @@ def main() -> int:
             return 2
         text += f"; 8-bit KV cache ({args.kv} codes, one scale per KV head)"
 
-    wl = build_workload(cfg, pos, args, args.kv, args.gemm)
+    wl = build_workload(cfg, pos, args, args.kv, args.gemm, mlp=args.mlp)
     nl, kb, step_bytes = wl["nl"], wl["kb"], wl["step_bytes"]
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.2f} GiB via torch + packed weights")
     t = time_workload(wl, args.steps, args.warmup, graph=not args.no_graph, samples=True)
     stream_ms, graph_ms, kern_us = t["stream_ms"], t["graph_ms"], t["kern_us"]
+    if args.mlp == "fused":   # the two MLP slots hold the fused kernel and the reduction
+        kb = dict(kb, mlp_fused=kb["mlp_gate_up"], mlp_reduce=kb["mlp_down"])
+        kern_us = {{"mlp_gate_up": "mlp_fused", "mlp_down": "mlp_reduce"}.get(k, k): v for k, v in kern_us.items()}
     log(f"stream: {stream_ms:.3f} ms/step, {stream_ms * 1e3 / nl:.2f} us/layer")
     log("kernels (us): " + ", ".join(f"{n} {v:.2f}" for n, v in kern_us.items()))
     if graph_ms is not None:
@@ -670,7 +680,7 @@ def main() -> int:
 
     workloads = None
     if not args.no_workloads and args.workload == "phi3_stack32_kv4k" and args.batch is None and not kv8 \
-            and args.gemm == "auto":
+            and args.gemm == "auto" and args.mlp == "split":
         log("other workloads (per layer step, rotating copies, HIP-graph replay)")
         workloads = other_workloads(args)
 
@@ -690,7 +700,7 @@ def main() -> int:
                                + ("" if cfg.layers > 1 else f" ({nl} rotating copies)"),
                    "layers": nl, "global_batch": cfg.batch, "seq_len": int(pos.max()) + 1,
                    "parallelism": "single GPU"},
-        "gemm_path": args.gemm, "kv_cache": args.kv,
+        "gemm_path": args.gemm, "mlp_path": args.mlp, "kv_cache": args.kv,
         "hbm_gbps": round(gbps, 1), "hbm_frac_of_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "read_ceiling": {"gbps": round(ceiling, 1),
                          "method": f"libfasttps_probe stream read of 4 GiB with 16-byte non-temporal loads, best "

@@ -225,6 +225,32 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
                                  with FASTTPS_ERR_UNSUPPORTED before any launch */
 FASTTPS_API int fasttps_set_gemm_path(fasttps_layer* layer, int32_t path);
 
+/* How the MLP (RMSNorm2, gate/up, siLu_Mul, down, residual) runs.
+ *   FASTTPS_MLP_SPLIT  (default) two kernels: gate/up with siLu_Mul stores
+ *                      h^sm (fp32, K values per sequence), the down
+ *                      projection reads it back with its residual (the
+ *                      structure of Alg. 4, which stores h^sm to L3 and loads
+ *                      it for the down projection)
+ *   FASTTPS_MLP_FUSED  the fused MLP of Section 3.2 with h^sm kept on chip:
+ *                      one kernel in which each block computes gate/up and
+ *                      siLu_Mul for a slice of the K units, keeps that slice
+ *                      in LDS and multiplies it with the matching columns of
+ *                      W_down into a partial of y; a second kernel adds the
+ *                      blocks' partials in a fixed order with the residual.
+ *                      Steps then run the vector projections (the matrix-core
+ *                      path is not used), and FASTTPS_DBG_MLP_A has nothing to
+ *                      read. Needs W_down in the kernel's slices, which
+ *                      fasttps_weights_pack stores (one more copy of W_down)
+ *                      only while this path is selected on the layer handle it
+ *                      packs with; a step with weights packed otherwise fails
+ *                      with FASTTPS_ERR_INVALID_ARG before any launch.
+ * Selecting FASTTPS_MLP_FUSED the first time allocates the partial sums
+ * (256 x max_batch x D fp32; blocking). Returns FASTTPS_ERR_INVALID_ARG for
+ * an unknown path, FASTTPS_ERR_OOM if the allocation fails. */
+#define FASTTPS_MLP_SPLIT 0
+#define FASTTPS_MLP_FUSED 1
+FASTTPS_API int fasttps_set_mlp_path(fasttps_layer* layer, int32_t path);
+
 /* Accuracy-study hook: when enabled, later steps of this layer handle round
  * the softmax weights to bf16 before the PV accumulation, as FlashAttention
  * does with its bf16 P (the softmax row sum stays fp32), so the attention

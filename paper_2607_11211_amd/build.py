@@ -20,7 +20,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfasttps.so")
 PROBE_LIB = os.path.join(PKG, "libfasttps_probe.so")
 
-SOURCES = ["gemv.hip", "mfma_proj.hip", "attention.hip", "fused_layer.hip", "pack.hip", "unfused.hip", "fasttps.cpp"]
+SOURCES = ["gemv.hip", "mlp_fused.hip", "mfma_proj.hip", "attention.hip", "fused_layer.hip", "pack.hip", "unfused.hip", "fasttps.cpp"]
 PROBE_SOURCES = ["stream_read.hip"]
 
 ARCH = "gfx950"

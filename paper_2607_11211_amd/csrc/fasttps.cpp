@@ -181,6 +181,11 @@ struct fasttps_layer {
   float* ssq_h1 = nullptr;
   int nbtc = 0;        // batch tiles of the operand buffers
   int gemm_path = FASTTPS_GEMM_AUTO;
+  // the MLP as one kernel with h^sm on chip (fasttps_set_mlp_path): its
+  // partial sums of y [slices][max_batch][D], allocated when first selected
+  int mlp_path = FASTTPS_MLP_SPLIT;
+  float* mlp_part = nullptr;
+  bool mlp_a_written = false;  // the last step stored h^sm (FASTTPS_DBG_MLP_A)
   // the fused kernel's phase hand-over: per-block phase flags, the epoch of
   // the last completed launch, the count of bounded waits that ran out
   unsigned* fused_flags = nullptr;
@@ -212,6 +217,9 @@ struct fasttps_weights {
   uint16_t* t_o = nullptr;
   uint16_t* t_gu = nullptr;
   uint16_t* t_down = nullptr;
+  // W_down in the fused MLP's slices [slices][D][u8], packed when the layer
+  // handle used for packing had the fused MLP selected; null otherwise
+  uint16_t* w_down_slices = nullptr;
 };
 
 namespace {
@@ -419,6 +427,10 @@ int fasttps_layer_destroy(fasttps_layer* l) {
   release_events(l);
   l->magic = kDeadMagic;
   hipError_t e = hipFree(l->arena);
+  if (l->mlp_part) {
+    const hipError_t e2 = hipFree(l->mlp_part);
+    if (e == hipSuccess) e = e2;
+  }
   if (l->uf_arena) {
     const hipError_t e2 = hipFree(l->uf_arena);
     if (e == hipSuccess) e = e2;
@@ -496,11 +508,14 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   const size_t n_qkv = (q + 2 * kv) * D, n_o = D * q, n_gu = 2 * K * D, n_d = K * D;
   const bool tiled = c.max_batch > 1;
   const LayerTiles lt = layer_tiles(c);
-  size_t offs[10], sizes[10] = {n_qkv * 2, n_o * 2, n_gu * 2, n_d * 2, D * 2, D * 2,
+  const bool slices = l->mlp_path == FASTTPS_MLP_FUSED;
+  const size_t n_sl = (size_t)mlp_fused_blocks((int)K) * D * mlp_fused_u8((int)K);
+  size_t offs[11], sizes[11] = {n_qkv * 2, n_o * 2, n_gu * 2, n_d * 2, D * 2, D * 2,
                                 tiled ? lt.qkv.elems() * 2 : 0, tiled ? lt.o.elems() * 2 : 0,
-                                tiled ? lt.gu.elems() * 2 : 0, tiled ? lt.down.elems() * 2 : 0};
+                                tiled ? lt.gu.elems() * 2 : 0, tiled ? lt.down.elems() * 2 : 0,
+                                slices ? n_sl * 2 : 0};
   size_t total = 0;
-  for (int i = 0; i < 10; ++i) {
+  for (int i = 0; i < 11; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -529,6 +544,7 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
     pw->t_gu = reinterpret_cast<uint16_t*>(base + offs[8]);
     pw->t_down = reinterpret_cast<uint16_t*>(base + offs[9]);
   }
+  if (slices) pw->w_down_slices = reinterpret_cast<uint16_t*>(base + offs[10]);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const auto* g = static_cast<const uint16_t*>(w->w_gate);
   const auto* u = static_cast<const uint16_t*>(w->w_up);
@@ -540,6 +556,7 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
       (e = hipMemcpyAsync(pw->mlp_norm, w->mlp_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, kInterlaceTile, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->w_down, w->w_down, n_d * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (slices && (e = launch_pack_down_slices(pw->w_down, pw->w_down_slices, (int)D, (int)K, s)) != hipSuccess) ||
       (tiled && ((e = launch_tile_weights(pw->w_qkv, nullptr, (int)(q + 2 * kv), (int)D, (int)D, lt.qkv.ns,
                                           lt.qkv.kt, lt.qkv.rh, pw->t_qkv, s)) != hipSuccess ||
                  (e = launch_tile_weights(pw->w_o, nullptr, (int)D, (int)q, (int)q, lt.o.ns, lt.o.kt, lt.o.rh,
@@ -694,8 +711,14 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   // fasttps_set_gemm_path says), where the weights carry MFMA tiles; the
   // allocation-free step runs the vector path
   const bool have_tiles = w->t_qkv != nullptr && l->op_o != nullptr;
-  const bool mfma = !S.noalloc && (l->gemm_path == FASTTPS_GEMM_MATRIX ||
-                                   (l->gemm_path == FASTTPS_GEMM_AUTO && have_tiles && batch >= kMfmaMinBatch));
+  // the fused MLP runs with the vector projections (and not in the
+  // allocation-free step)
+  const bool mlp_fused = !S.noalloc && l->mlp_path == FASTTPS_MLP_FUSED;
+  if (mlp_fused && !w->w_down_slices)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the fused MLP needs weights packed while it was selected on the layer");
+  const bool mfma = !S.noalloc && !mlp_fused &&
+                    (l->gemm_path == FASTTPS_GEMM_MATRIX ||
+                     (l->gemm_path == FASTTPS_GEMM_AUTO && have_tiles && batch >= kMfmaMinBatch));
   if (mfma && !have_tiles)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
 
@@ -715,7 +738,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   fsh.down = gemv_shape_b1(c.intermediate, false);
   const bool fused_ok = batch == 1 && kvf == kKvBf16 && l->p_bf16 == 0 && nsplit <= 64 &&
                         ceil_div(c.n_heads * (int)d, kFusedBlocks) * nsplit <= 1024 && fused_layer_supported(fsh);
-  const bool fused = !mfma && !S.noalloc && l->gemm_path == FASTTPS_GEMM_FUSED;
+  const bool fused = !mfma && !S.noalloc && !mlp_fused && l->gemm_path == FASTTPS_GEMM_FUSED;
   if (fused && !fused_ok)
     return fail(FASTTPS_ERR_UNSUPPORTED, "the fused kernel is built for one sequence of the Phi-3-mini layer shape");
 
@@ -805,7 +828,10 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   for (int b = 0; b < batch; ++b) aa.order.p[b] = b;
   std::stable_sort(aa.order.p, aa.order.p + batch, [&](int32_t u, int32_t v) { return pos[u] > pos[v]; });
 
-  if (!S.noalloc) l->dbg_written = 0;
+  if (!S.noalloc) {
+    l->dbg_written = 0;
+    l->mlp_a_written = !mlp_fused;  // h^sm is stored by every path but the fused MLP
+  }
   if (fused) {
     FusedArgs f{};
     f.qkv = qa;
@@ -884,8 +910,20 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     if ((e = launch_mfma_down(m, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
   } else {
     if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
-    if ((e = launch_gate_up(ga, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
-    if ((e = launch_down_residual(da, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
+    if (mlp_fused) {
+      MlpFusedArgs mf{};
+      mf.w_down_slices = w->w_down_slices;
+      mf.part = l->mlp_part;
+      mf.y = static_cast<uint16_t*>(y);
+      mf.nblk = mlp_fused_blocks(c.intermediate);
+      mf.u8 = mlp_fused_u8(c.intermediate);
+      mf.hidden = (int)D;
+      mf.batch = batch;
+      if ((e = launch_mlp_fused(ga, mf, s, ev[4], ev[5])) != hipSuccess) return hip_fail(e, "fused mlp launch");
+    } else {
+      if ((e = launch_gate_up(ga, s, ev[4])) != hipSuccess) return hip_fail(e, "mlp gate/up launch");
+      if ((e = launch_down_residual(da, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
+    }
   }
   used(3);
   used(4);
@@ -963,7 +1001,12 @@ int fasttps_debug_read(fasttps_layer* l, int32_t which, int32_t batch, void* dst
     case FASTTPS_DBG_QKV: src = l->qkv; n = (size_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim; break;
     case FASTTPS_DBG_ATTN: src = l->attn_o; n = (size_t)c.n_heads * c.head_dim; break;
     case FASTTPS_DBG_H1: src = l->h1; n = (size_t)c.hidden; break;
-    case FASTTPS_DBG_MLP_A: src = l->mlp_a; n = (size_t)c.intermediate; break;
+    case FASTTPS_DBG_MLP_A:
+      if (!l->mlp_a_written)
+        return fail(FASTTPS_ERR_INVALID_ARG, "the last step kept h^sm on chip (fused MLP): nothing to read");
+      src = l->mlp_a;
+      n = (size_t)c.intermediate;
+      break;
     case FASTTPS_DBG_FUSED_WAITS: src = l->fused_err; n = 1; batch = 1; break;
     case FASTTPS_DBG_QK_ROPE:
     case FASTTPS_DBG_H:
@@ -1081,6 +1124,26 @@ int fasttps_set_gemm_path(fasttps_layer* l, int32_t path) {
   if (path == FASTTPS_GEMM_MATRIX && !l->op_o)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer with max_batch > 1");
   l->gemm_path = path;
+  return FASTTPS_OK;
+}
+
+int fasttps_set_mlp_path(fasttps_layer* l, int32_t path) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (path != FASTTPS_MLP_SPLIT && path != FASTTPS_MLP_FUSED)
+    return fail(FASTTPS_ERR_INVALID_ARG, "unknown MLP path %d", path);
+  if (path == FASTTPS_MLP_FUSED && !l->mlp_part) {
+    const fasttps_config& c = l->cfg;
+    const size_t bytes = (size_t)mlp_fused_blocks(c.intermediate) * c.max_batch * c.hidden * sizeof(float);
+    void* p = nullptr;
+    const hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(FASTTPS_ERR_OOM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+    }
+    l->mlp_part = static_cast<float*>(p);
+  }
+  l->mlp_path = path;
   return FASTTPS_OK;
 }
 

@@ -58,6 +58,22 @@ hipError_t launch_gate_up(const GemvArgs& a, hipStream_t s, KernelEvents ev = {}
 // out = W act (fp32 in and out), rows of `ld` elements (the op-by-op baseline).
 hipError_t launch_gemv_plain(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
+// The fused MLP (mlp_fused.hip): gate/up + siLu_Mul of a slice of units per
+// block with h^sm kept in LDS, the slice's down-projection partial of y, and
+// a fixed-order sum of the partials with the residual.
+struct MlpFusedArgs {
+  const uint16_t* w_down_slices;  // [nblk][hidden][u8] bf16 (launch_pack_down_slices)
+  float* part;                    // [nblk][batch][hidden] fp32 partials of W_down a
+  uint16_t* y;                    // [batch][hidden] bf16 output
+  int nblk, u8, hidden, batch;
+};
+int mlp_fused_blocks(int inter);  // blocks (slices) of the fused MLP
+int mlp_fused_u8(int inter);      // units per slice, rounded up to a multiple of 8
+// a: the gate/up GemvArgs (w = interlaced W_gu, in_f32 = h1, gamma = RMSNorm2 gain)
+hipError_t launch_mlp_fused(const GemvArgs& a, const MlpFusedArgs& m, hipStream_t s, KernelEvents ev_slice = {},
+                            KernelEvents ev_reduce = {});
+hipError_t launch_pack_down_slices(const uint16_t* w_down, uint16_t* dst, int hidden, int inter, hipStream_t s);
+
 // Batched projections on the matrix cores: out = W act over weights packed
 // in MFMA tiles (16 rows x 32 inputs, 1 KB, in operand order) and
 // activations split into two bf16 levels (see mfma_proj.hip).

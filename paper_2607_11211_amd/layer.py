@@ -29,6 +29,7 @@ DBG_QKV, DBG_ATTN, DBG_H1, DBG_MLP_A, DBG_FUSED_WAITS = 0, 1, 2, 3, 4
 DBG_QK_ROPE, DBG_H, DBG_H2 = 5, 6, 7
 
 GEMM_AUTO, GEMM_VECTOR, GEMM_MATRIX, GEMM_FUSED = 0, 1, 2, 3
+MLP_SPLIT, MLP_FUSED = 0, 1
 
 KV_FP8_E4M3 = 1
 KV_INT8 = 2
@@ -38,7 +39,7 @@ EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step"
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
            "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_set_debug", "fasttps_validate_step",
-           "fasttps_decode_step_noalloc",
+           "fasttps_set_mlp_path", "fasttps_decode_step_noalloc",
            "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 7
 
@@ -69,15 +70,16 @@ def _load() -> ctypes.CDLL:
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     lib.fasttps_layer_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]
     lib.fasttps_weights_pack.argtypes = [vp, ctypes.POINTER(WeightsDesc), vp, ctypes.POINTER(vp)]
-    lib.fasttps_decode_step.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
-    lib.fasttps_decode_step_unfused.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
-    lib.fasttps_decode_step_noalloc.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, vp, vp, vp, vp]
+    lib.fasttps_decode_step.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.fasttps_decode_step_unfused.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.fasttps_decode_step_noalloc.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, vp]
     fp = ctypes.POINTER(ctypes.c_float)
-    lib.fasttps_decode_step_kv8.argtypes = [vp, vp, vp, ctypes.POINTER(i32), i32, i32, vp, vp, fp, fp, vp, vp]
+    lib.fasttps_decode_step_kv8.argtypes = [vp, vp, vp, vp, i32, i32, vp, vp, fp, fp, vp, vp]
     lib.fasttps_unfused_enable.argtypes = [vp]
     lib.fasttps_set_attention_p_bf16.argtypes = [vp, i32]
     lib.fasttps_set_gemm_path.argtypes = [vp, i32]
     lib.fasttps_set_debug.argtypes = [vp, i32]
+    lib.fasttps_set_mlp_path.argtypes = [vp, i32]
     lib.fasttps_validate_step.argtypes = [ctypes.POINTER(Config), vp, ctypes.POINTER(i32), i32, vp, vp, vp, i32]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
@@ -94,7 +96,8 @@ def _load() -> ctypes.CDLL:
                  "fasttps_profile_begin", "fasttps_profile_end", "fasttps_weights_free",
                  "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
                  "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8", "fasttps_set_gemm_path",
-                 "fasttps_set_debug", "fasttps_validate_step", "fasttps_decode_step_noalloc"):
+                 "fasttps_set_debug", "fasttps_validate_step", "fasttps_decode_step_noalloc",
+                 "fasttps_set_mlp_path"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -141,7 +144,7 @@ def _stream_handle(stream) -> Optional[int]:
     if stream is None:
         import torch
         stream = torch.cuda.current_stream()
-    return int(stream.cuda_stream) or None
+    return stream.cuda_stream or None
 
 
 class Weights:
@@ -175,25 +178,44 @@ class Layer:
         h = ctypes.c_void_p()
         _check(LIB.fasttps_layer_create(ctypes.byref(self.c), ctypes.byref(h)), "fasttps_layer_create")
         self.handle = h
+        self._h = h.value
+        # host staging of the positions a step passes (read by the call itself)
+        self._pos = (ctypes.c_int32 * 64)()
+        self._pos_addr = ctypes.addressof(self._pos)
+
+    def _stage_pos(self, pos):
+        """Host address and length of pos (int32) for a step call: copied into
+        the handle's staging array (the library reads it during the call, so
+        one array serves every call); past 64 entries into a fresh array, for
+        the library to refuse."""
+        vals = pos.tolist() if isinstance(pos, np.ndarray) else list(pos)
+        n = len(vals)
+        if n > 64:
+            self._pos_big = (ctypes.c_int32 * n)(*vals)
+            return ctypes.addressof(self._pos_big), n
+        buf = self._pos
+        for i, v in enumerate(vals):
+            buf[i] = v
+        return self._pos_addr, n
 
     def pack(self, tensors: Dict[str, "object"], stream=None) -> Weights:
         return Weights(self, tensors, stream)
 
     def step(self, weights: Weights, x, pos, k_cache, v_cache, y, stream=None) -> None:
-        """Enqueue one decode step. pos: host ints [batch]; tensors: torch device tensors."""
-        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
-        batch = int(p.shape[0])
-        _check(LIB.fasttps_decode_step(self.handle, weights.handle, _ptr(x),
-                                       p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
-                                       _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
-               "fasttps_decode_step")
+        """Enqueue one decode step. pos: host ints [batch]; tensors: torch device tensors.
+        (Kept lean: on a 32-layer stack the host issues every layer's step.)"""
+        pa, n = self._stage_pos(pos)
+        st = LIB.fasttps_decode_step(self._h, weights.handle, x.data_ptr(), pa, n,
+                                     k_cache.data_ptr(), v_cache.data_ptr(), y.data_ptr(),
+                                     _stream_handle(stream))
+        if st:
+            _check(st, "fasttps_decode_step")
 
     def step_noalloc(self, weights: Weights, x, pos, k_cache, v_cache, y, stream=None) -> None:
         """Enqueue one decode step that allocates nothing (the library's static
         scratch array; vector-path kernels). Same contract as step."""
-        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
-        _check(LIB.fasttps_decode_step_noalloc(self.handle, weights.handle, _ptr(x),
-                                               p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(p.shape[0]),
+        pa, n = self._stage_pos(pos)
+        _check(LIB.fasttps_decode_step_noalloc(self._h, weights.handle, _ptr(x), pa, n,
                                                _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step_noalloc")
 
@@ -206,14 +228,13 @@ class Layer:
         """
         if fmt not in KV_FORMATS:
             raise ValueError(f"unknown 8-bit KV format {fmt!r}")
-        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
+        pa, n = self._stage_pos(pos)
         ks = np.ascontiguousarray(np.asarray(k_scale, dtype=np.float32))
         vs = np.ascontiguousarray(np.asarray(v_scale, dtype=np.float32))
         if ks.shape != (self.cfg.n_kv_heads,) or vs.shape != (self.cfg.n_kv_heads,):
             raise ValueError(f"scales must have shape ({self.cfg.n_kv_heads},)")
         fptr = ctypes.POINTER(ctypes.c_float)
-        _check(LIB.fasttps_decode_step_kv8(self.handle, weights.handle, _ptr(x),
-                                           p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(p.shape[0]),
+        _check(LIB.fasttps_decode_step_kv8(self._h, weights.handle, _ptr(x), pa, n,
                                            KV_FORMATS[fmt], _ptr(k_cache), _ptr(v_cache),
                                            ks.ctypes.data_as(fptr), vs.ctypes.data_as(fptr), _ptr(y),
                                            _stream_handle(stream)),
@@ -225,10 +246,8 @@ class Layer:
 
     def step_unfused(self, weights: Weights, x, pos, k_cache, v_cache, y, stream=None) -> None:
         """Enqueue one step of the op-by-op baseline (same contract as step)."""
-        p = np.ascontiguousarray(np.asarray(pos, dtype=np.int32))
-        batch = int(p.shape[0])
-        _check(LIB.fasttps_decode_step_unfused(self.handle, weights.handle, _ptr(x),
-                                               p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), batch,
+        pa, n = self._stage_pos(pos)
+        _check(LIB.fasttps_decode_step_unfused(self._h, weights.handle, _ptr(x), pa, n,
                                                _ptr(k_cache), _ptr(v_cache), _ptr(y), _stream_handle(stream)),
                "fasttps_decode_step_unfused")
 
@@ -245,6 +264,11 @@ class Layer:
                "fasttps_debug_read")
         torch.cuda.synchronize()
         return int(t.item())
+
+    def set_mlp_path(self, path: int) -> None:
+        """MLP_SPLIT (gate/up stores h^sm, down reads it) or MLP_FUSED (h^sm kept on chip;
+        weights must be packed after selecting it)."""
+        _check(LIB.fasttps_set_mlp_path(self.handle, int(path)), "fasttps_set_mlp_path")
 
     def set_debug(self, enable: bool) -> None:
         """Test hook: later steps also write q, k after RoPE and the two normalized activations."""
@@ -274,6 +298,7 @@ class Layer:
         if self.handle:
             _check(LIB.fasttps_layer_destroy(self.handle), "fasttps_layer_destroy")
             self.handle = None
+            self._h = None
 
     def __del__(self):
         try:
