@@ -78,15 +78,19 @@ __device__ __forceinline__ void attn_split_body(const AttnArgs& a, float kscale,
   body.run(kscale, vscale);
 }
 
+// At least two waves per SIMD: the groups of four at d = 128 (one tile in
+// flight per lane, o of four heads in registers) then fit 256 registers
+// without spilling, so two blocks share a CU instead of one.
 template <int D, int G, int NRING, bool PBF16, bool XCH>
-__global__ __launch_bounds__(kThreads) void attn_split_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void attn_split_kernel(AttnArgs a) {
   attn_split_body<D, G, NRING, PBF16, kKvBf16, XCH>(a, 1.f, 1.f);
 }
 
 // 8-bit cache: the KV head's two scales come from the argument block; tiles
 // in flight as for a bf16 cache
 template <int D, int G, int KVF>
-__global__ __launch_bounds__(kThreads) void attn_split_kv8_kernel(AttnArgs a, KvScales sc) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void attn_split_kv8_kernel(
+    AttnArgs a, KvScales sc) {
   attn_split_body<D, G, (G <= 2 ? 2 : 1), false, KVF, false>(a, sc.k[blockIdx.y], sc.v[blockIdx.y]);
 }
 
@@ -233,12 +237,13 @@ hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   int maxp = 0;
   for (int b = 0; b < a.batch; ++b) maxp = a.pos.p[b] > maxp ? a.pos.p[b] : maxp;
   const int tiles = (maxp + attn::kTile - 1) / attn::kTile;
-  const bool xch = G <= 2 && (tiles + a.nsplit - 1) / a.nsplit >= kXchMinTiles;
-  if (a.p_bf16)
-    return xch ? ext_launch(attn_split_kernel<D, G, NRING, true, true>, grid, dim3(kThreads), 0, s, ev, a)
-               : ext_launch(attn_split_kernel<D, G, NRING, true, false>, grid, dim3(kThreads), 0, s, ev, a);
-  return xch ? ext_launch(attn_split_kernel<D, G, NRING, false, true>, grid, dim3(kThreads), 0, s, ev, a)
-             : ext_launch(attn_split_kernel<D, G, NRING, false, false>, grid, dim3(kThreads), 0, s, ev, a);
+  if constexpr (G <= 2) {
+    if ((tiles + a.nsplit - 1) / a.nsplit >= kXchMinTiles)
+      return a.p_bf16 ? ext_launch(attn_split_kernel<D, G, NRING, true, true>, grid, dim3(kThreads), 0, s, ev, a)
+                      : ext_launch(attn_split_kernel<D, G, NRING, false, true>, grid, dim3(kThreads), 0, s, ev, a);
+  }
+  return a.p_bf16 ? ext_launch(attn_split_kernel<D, G, NRING, true, false>, grid, dim3(kThreads), 0, s, ev, a)
+                  : ext_launch(attn_split_kernel<D, G, NRING, false, false>, grid, dim3(kThreads), 0, s, ev, a);
 }
 
 template <int D, int G>
