@@ -151,10 +151,10 @@ FASTTPS_API int fasttps_decode_step_noalloc(fasttps_layer* layer, const fasttps_
 #define FASTTPS_KV_INT8 2     /* two's complement, entries in [-127, 127] */
 
 /* One decode step over an 8-bit KV cache. The paper holds its cache layout
- * and append compatible with a quantized cache (Section 6.2, and Section 2.4,
- * which counts the quantized cache's concatenation among the memory
- * reorganisation operators) without fixing a format; this is the reading
- * implemented:
+ * and append compatible with a quantized cache (Section 5.2, Compatibility
+ * with Acceleration Algorithm; Section 2.4, Operator Type and OI, counts the
+ * quantized cache's concatenation among the memory reorganisation
+ * operators) without fixing a format; this is the reading implemented:
  *   kv_format  FASTTPS_KV_FP8_E4M3 or FASTTPS_KV_INT8
  *   k_cache, v_cache
  *              device, [batch, H_kv, N_max, d] of 8-bit codes, the GKVC layout
@@ -210,7 +210,7 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
  *   FASTTPS_GEMM_AUTO    (default) the matrix path from 2 sequences up where
  *                        the weights carry the tiles, else the vector path
  * At batch 8-16 the projections are dense enough that the multiply-adds
- * outgrow the vector ALUs beside the weight stream (Section 4.4 puts the
+ * outgrow the vector ALUs beside the weight stream (Section 4.4, OI and Accuracy, puts the
  * token-phase projections at the weight stream); both paths read every
  * weight once per step. Returns FASTTPS_ERR_INVALID_ARG for an unknown path,
  * or for FASTTPS_GEMM_MATRIX on a layer with max_batch == 1. A step with the
@@ -255,7 +255,7 @@ FASTTPS_API int fasttps_set_mlp_path(fasttps_layer* layer, int32_t path);
  * the softmax weights to bf16 before the PV accumulation, as FlashAttention
  * does with its bf16 P (the softmax row sum stays fp32), so the attention
  * output error of the two can be compared over the context length (the
- * paper's Fig. 8 comparison, Section 5.4). Off by default; a step with it on
+ * paper's Fig. 8 comparison, Section 4.4, OI and Accuracy). Off by default; a step with it on
  * is not the FastTPS step. */
 FASTTPS_API int fasttps_set_attention_p_bf16(fasttps_layer* layer, int32_t enable);
 

@@ -1,9 +1,9 @@
 """8-bit KV cache formats for the fp64 oracle (test infrastructure only).
 
 The paper states that its cache management works unchanged with a quantized
-KV cache (Section 6.2; Section 2.4 counts the concatenation of a quantized
-cache among the memory-reorganisation operators) but fixes no format. The
-reading used here:
+KV cache (Section 5.2, Compatibility with Acceleration Algorithm; Section 2.4,
+Operator Type and OI, counts the concatenation of a quantized cache among the
+memory-reorganisation operators) but fixes no format. The reading used here:
 
   * an entry's d values are stored as 8-bit codes, FP8 E4M3 (the OCP
     "e4m3fn" encoding: 1 sign, 4 exponent bits with bias 7, 3 mantissa bits;

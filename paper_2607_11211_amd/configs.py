@@ -1,6 +1,6 @@
 """Workload shapes for one token-phase decoder layer.
 
-The shapes follow the model table of the FastTPS paper (Section 5.1, Table 1):
+The shapes follow the model table of the FastTPS paper (Section 4.1, Faster Attention Block, Table 1):
 the Phi-3-mini column gives 32 query heads = 32 KV heads, head dim 96, MLP width
 8192 (hidden 3072 = 32 x 96); the Llama3 column gives 32 query heads over 8 KV
 heads, head dim 128, MLP width 14336. Every workload here is synthetic: weights,

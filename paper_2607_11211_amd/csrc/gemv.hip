@@ -4,7 +4,7 @@
 // the residual and the bf16 rounding of y.
 //
 // At batch 1-8 the projections are matrix-vector products whose cost is the
-// bf16 weight stream from HBM (Section 4.4 of the paper: token-phase MLP and
+// bf16 weight stream from HBM (Section 4.4 of the paper, OI and Accuracy: token-phase MLP and
 // projections are bound by weight movement). Layout of the work:
 //   * rows are dealt to the blocks round-robin (block b takes rows b, b + G,
 //     b + 2G, ... of a grid of G blocks), so at any moment the chip reads a

@@ -1,5 +1,5 @@
 """Attention-output accuracy against fp64 over the context length (the
-paper's Fig. 8 study, Section 5.4), on MI355X through the C ABI.
+paper's Fig. 8 study, Section 4.4, OI and Accuracy), on MI355X through the C ABI.
 
 For N_t = pos + 1 from 128 to 32768 cached entries at the Phi-3 attention
 shape (32 heads of 96), the step's attention output o (fp32) is compared with
