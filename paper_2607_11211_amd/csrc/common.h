@@ -22,6 +22,28 @@ __device__ __forceinline__ T ld_stream(const T* p) {
   return __builtin_nontemporal_load(p);
 }
 
+// ---- data handed between blocks of one launch ----------------------------
+// The L2 caches are per XCD and not coherent with each other. Data another
+// block reads in the same launch is stored and loaded with the accesses of
+// relaxed agent-scope atomics (global_store / global_load sc1), which bypass
+// the non-coherent L2, so no L2 write-back or invalidate is needed; the
+// writer waits for its stores (wait_vm) before it signals.
+__device__ __forceinline__ float ld_c(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_c(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned ld_cu(const unsigned* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_cu(unsigned* p, unsigned v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// wait for this wave's outstanding memory operations, stores included
+// (s_waitcnt vmcnt(0); expcnt and lgkmcnt left free)
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // ---- bfloat16 <-> float -------------------------------------------------
 // bf16 is the upper half of a binary32, so widening is a shift.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -180,6 +180,9 @@ struct fasttps_layer {
   uint16_t* op_down = nullptr;
   float* ssq_h1 = nullptr;
   int nbtc = 0;        // batch tiles of the operand buffers
+  float* split_part = nullptr;    // the split projections' partial sums
+  unsigned* split_tickets = nullptr;  // and their row groups' tickets (zero between steps)
+  size_t split_part_cap = 0, split_tickets_cap = 0;
   int gemm_path = FASTTPS_GEMM_AUTO;
   // the MLP as one kernel with h^sm on chip (fasttps_set_mlp_path): its
   // partial sums of y [slices][max_batch][D], allocated when first selected
@@ -334,7 +337,18 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
   const bool mfma = B > 1;
   const int nbtc = 2 * ceil_div(B, 16);
   const LayerTiles lt = layer_tiles(c);
-  size_t sizes[15] = {
+  // the split projections run one after another: one scratch serves them all
+  size_t split_floats = 0, split_tickets = 0;
+  if (mfma) {
+    const TileDims* tds[3] = {&lt.o, &lt.gu, &lt.down};
+    for (int i = 0; i < 3; ++i) {
+      size_t f = 0, t = 0;
+      mfma_split_need(i + 1, tds[i]->ns, tds[i]->kt, tds[i]->rh, B, &f, &t);
+      split_floats = std::max(split_floats, f);
+      split_tickets = std::max(split_tickets, t);
+    }
+  }
+  size_t sizes[17] = {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
@@ -350,9 +364,11 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
       (size_t)B * (c.n_heads + c.n_kv_heads) * d * sizeof(float),
       (size_t)B * c.hidden * sizeof(float),
       (size_t)B * c.hidden * sizeof(float),
+      split_floats * sizeof(float),
+      split_tickets * sizeof(unsigned),
   };
-  size_t total = 0, offs[15];
-  for (int i = 0; i < 15; ++i) {
+  size_t total = 0, offs[17];
+  for (int i = 0; i < 17; ++i) {
     offs[i] = total;
     total += align256(sizes[i]);
   }
@@ -395,6 +411,12 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
     l->op_down = reinterpret_cast<uint16_t*>(base + offs[9]);
     l->ssq_h1 = reinterpret_cast<float*>(base + offs[10]);
     l->nbtc = nbtc;
+    if (split_floats && split_tickets) {
+      l->split_part = reinterpret_cast<float*>(base + offs[15]);
+      l->split_tickets = reinterpret_cast<unsigned*>(base + offs[16]);
+      l->split_part_cap = split_floats;
+      l->split_tickets_cap = split_tickets;
+    }
   }
   l->fused_flags = reinterpret_cast<unsigned*>(base + offs[11]);
   l->fused_epoch = l->fused_flags + kFusedPhases * kFusedBlocks;
@@ -867,6 +889,10 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     m.nbtc = l->nbtc;
     m.a_out_nbtc = l->nbtc;
     m.eps = c.rms_eps;
+    m.kpart = l->split_part;
+    m.tickets = l->split_tickets;
+    m.kpart_cap = l->split_part_cap;
+    m.tickets_cap = l->split_tickets_cap;
     return m;
   };
 

@@ -53,21 +53,6 @@ constexpr size_t kMaxFusedLds = 160 * 1024;
 constexpr int kFusedGrid = 256;                      // one block per CU
 constexpr int kFlagsPerLane = kFusedGrid / kWave;     // a wave polls the grid's flags
 
-__device__ __forceinline__ float ld_c(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_c(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ unsigned ld_cu(const unsigned* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_cu(unsigned* p, unsigned v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// wait for this wave's outstanding memory operations (vmcnt(0))
-__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
 // GEMV IO of the fused kernel: activation from the LDS stage, residual and
 // fp32 outputs coherent
 struct FusedGemvIO {

@@ -96,7 +96,17 @@ struct MfmaArgs {
   const float* res_f32;     // down: residual h1 [batch, rows]
   uint16_t* out_bf16;       // down: y [batch, rows] bf16
   float eps;
+  // split inputs (O, gate/up, down): scratch for the parts' fp32 partial sums
+  // and the row groups' tickets (zero between launches; every launch leaves
+  // them zero), with their sizes (mfma_split_need); null: no split
+  float* kpart;
+  unsigned* tickets;
+  size_t kpart_cap, tickets_cap;
+  int ks, ktq, kstride;     // set by the launcher: parts, k-tiles per part, floats per block of kpart
 };
+// the split scratch a projection needs at up to `batch` sequences (mode 0
+// QKV, 1 O, 2 gate/up, 3 down; ns stripes of rh rows and kt k-tiles)
+void mfma_split_need(int mode, int ns, int kt, int rh, int batch, size_t* kpart_floats, size_t* tickets);
 hipError_t launch_mfma_qkv(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});
 hipError_t launch_mfma_oproj(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});
 hipError_t launch_mfma_gate_up(const MfmaArgs& a, hipStream_t s, KernelEvents ev = {});

@@ -62,8 +62,14 @@ constexpr int kGroupSeq = 16;     // sequences per block row of the grid (two ba
 constexpr int kMaxStripesIn = 1024;  // stripes of the O projection's sums of squares (D <= 8192 at 8 rows)
 constexpr int kMaxChunkBytes = 40 * 1024;  // LDS for the partial sums of one chunk of stripes
 constexpr int kMaxHidden = 8192;           // inputs of the QKV projection (gamma1 in LDS)
+constexpr int kMaxParts = 4;               // input parts of a split projection
 
 enum class MMode { kQkv, kOproj, kGateUp, kDown };
+
+template <int V>
+struct SlotBase {
+  static constexpr int value = V;
+};
 
 __device__ __forceinline__ bf16x8 as_bf16x8(v4u v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -108,7 +114,11 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   constexpr bool CACHED = NT > 0;
   constexpr int NOUT = NBT * kSeqTile * 16;  // (sequence, column) slots of a stripe
   static_assert(kMT % NOUT == 0, "epilogue slots");
-  static_assert(!CACHED || NT % NBUF == 0, "static ring slots");
+  // cached: the ring holds part of one stripe's run (NT % NBUF == 0) or the
+  // runs of two stripes (NBUF == 2 NT); either way ring slots are static
+  static_assert(!CACHED || NT % NBUF == 0 || NBUF == 2 * NT, "static ring slots");
+  constexpr int SPR = CACHED && NBUF > NT ? 2 : 1;  // stripes per pass of the ring
+  constexpr int RB = NBUF / SPR;                     // ring slots per stripe
   extern __shared__ float red[];                // [a.sch][kMW][NOUT]: per wave, level-summed
   __shared__ float ssq[kMW][NBT * kSeqTile];    // per-wave sums of squares (QKV, gate/up)
   __shared__ v4u gam[MODE == MMode::kQkv ? kMaxHidden / 8 : 1];  // QKV: gamma1
@@ -117,12 +127,18 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   const int lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: scalar loop control
   const int G = gridDim.x, blk = blockIdx.x;
+  // split inputs: block blk is part kq of row group rg; the ks blocks of a
+  // group take the same stripes over disjoint ranges of k-tiles
+  const int ks = a.ks;
+  const int rg = blk / ks, kq = blk - rg * ks;
+  const int NGr = G / ks;                             // row groups
   const int b0 = blockIdx.y * kGroupSeq;              // first sequence of this grid row
   const int nb = min(NBT * kSeqTile, a.batch - b0);   // sequences of this grid row
-  const int nstr = (a.ns - 1 - blk) / G + 1;          // stripes blk, blk + G, ... (>= 1)
+  const int nstr = (a.ns - 1 - rg) / NGr + 1;         // stripes rg, rg + NGr, ... (>= 1)
   const int nt = CACHED ? NT : a.nt;
   const int ntp = CACHED ? NT : (nt + NBUF - 1) / NBUF * NBUF;
-  const int tbase = wave * nt;
+  const int kbeg = kq * a.ktq, kend = min(kbeg + a.ktq, a.kt);  // this part's k-tiles
+  const int tbase = kbeg + wave * nt;
   const int R = a.rh;                                  // rows per stripe (<= 16)
   const int n16 = lane & 15, kg = lane >> 4;
   const int bp = n16 >> 1, lvl = lane & 1;
@@ -202,8 +218,8 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   v4u ar[CACHED ? 1 : NBUF][NBT];  // streamed: ready operand, or (QKV) the x chunk
   auto load_item = [&](int r, int j) {
     const int si = min(j / ntp, nstr - 1);
-    const int t = min(tbase + j % ntp, a.kt - 1);
-    const int s = blk + si * G;
+    const int t = min(tbase + j % ntp, kend - 1);
+    const int s = rg + si * NGr;
     wr[r] = ld_stream(W + (((size_t)s * a.kt + t) * 4 + kg) * R + min(n16, R - 1));
     if constexpr (!CACHED) {
       if (MODE == MMode::kQkv) {
@@ -236,7 +252,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-      for (int bt = 0; bt < NBT; ++bt) acache[tt][bt] = tbase + tt < a.kt ? acache[tt][bt] : z;
+      for (int bt = 0; bt < NBT; ++bt) acache[tt][bt] = tbase + tt < kend ? acache[tt][bt] : z;
   }
   if (MODE == MMode::kGateUp) {
     // the wave's share of RMSNorm2's sums (loads issued first, so this waits
@@ -250,14 +266,71 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   // ---- stream the stripes; partial sums go to LDS, summed per chunk ------
   float inv = 1.f;  // the norm factor of this thread's epilogue sequence
   int c0 = 0;       // first stripe of the current chunk
-  for (int si = 0; si < nstr; ++si) {
+  constexpr int NCOL = 16;
+  // RMSNorm's factor for this thread's epilogue sequence, from the per-wave
+  // sums of squares in LDS
+  auto norm_factor = [&]() {
+    const int bl = min(tid % NOUT / NCOL, nb - 1);
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < kMW; ++w) t += ssq[w][bl];
+    return 1.0f / sqrtf(t / (float)a.din + a.eps);
+  };
+  // the mode's epilogue for slot o (sequence o / NCOL, column o % NCOL) of
+  // stripe s; col(cc) is the finished sum of column cc for that sequence
+  auto finish = [&](int s, int o, auto col) {
+    const int bl = min(o / NCOL, nb - 1);
+    const int b = b0 + bl;
+    if (MODE == MMode::kGateUp) {
+      const int U = R / 2;  // units per stripe: gate columns [0, U), up columns [U, 2U)
+      const int nreal = min(U, a.rows - U * s);
+      const int n = min(o % NCOL, nreal - 1);
+      const int u = U * s + n;
+      const float gt = inv * col(n), up = inv * col(n + U);
+      const float av = gt / (1.0f + expf(-gt)) * up;
+      a.out[(size_t)b * a.rows + u] = av;
+      const uint32_t hi = bf16_bits(av);
+      const uint32_t lo = bf16_bits(av - __uint_as_float(hi << 16));
+      a.a_out[operand_offset(b, u, 0, a.a_out_nbtc)] = (uint16_t)hi;
+      a.a_out[operand_offset(b, u, 1, a.a_out_nbtc)] = (uint16_t)lo;
+    } else {
+      const int nreal = min(R, a.rows - R * s);
+      const int n = min(o % NCOL, nreal - 1);
+      const int row = R * s + n;
+      const size_t oi = (size_t)b * a.rows + row;
+      if (MODE == MMode::kQkv) {
+        a.out[oi] = inv * col(n);
+      } else if (MODE == MMode::kOproj) {
+        const float h1 = bf16_to_f32(a.x_bf16[oi]) + col(n);
+        a.out[oi] = h1;
+        // the gate/up operand: split of h1 * gamma2 at input `row`
+        const float hg = h1 * bf16_to_f32(a.gamma[row]);
+        const uint32_t hi = bf16_bits(hg);
+        const uint32_t lo = bf16_bits(hg - __uint_as_float(hi << 16));
+        a.a_out[operand_offset(b, row, 0, a.a_out_nbtc)] = (uint16_t)hi;
+        a.a_out[operand_offset(b, row, 1, a.a_out_nbtc)] = (uint16_t)lo;
+        // this stripe's sum of h1^2 per sequence (the 16 columns are one DPP row)
+        float sq = o % NCOL < nreal ? h1 * h1 : 0.f;
+        sq = row_stride4_sum(quad_sum(sq));
+        a.ssq_out[(size_t)s * a.batch + b] = sq;
+      } else {
+        a.out_bf16[oi] = f32_to_bf16(a.res_f32[oi] + col(n));
+      }
+    }
+  };
+  // split inputs: this block's partial sums [stripe][slot]
+  float* kp_own = a.kpart + ((size_t)blockIdx.y * G + blk) * a.kstride;
+  // stripe si, whose items use ring slots SB .. SB + RB - 1 (SB: a constant)
+  auto stripe = [&](int si, auto sb) {
+    constexpr int SB = decltype(sb)::value;
     f4 acc[NBT];
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) acc[bt] = f4{0.f, 0.f, 0.f, 0.f};
-    for (int tt0 = 0; tt0 < ntp; tt0 += NBUF) {
+    for (int tt0 = 0; tt0 < ntp; tt0 += RB) {
 #pragma unroll
-      for (int r = 0; r < NBUF; ++r) {
-        const int tt = tt0 + r;
+      for (int rr = 0; rr < RB; ++rr) {
+        const int r = SB + rr;
+        const int tt = tt0 + rr;
         bf16x8 A[NBT];
         if constexpr (CACHED) {
 #pragma unroll
@@ -271,7 +344,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
           }
         } else {
           const int t = tbase + tt;
-          const bool live = tt < nt && t < a.kt;
+          const bool live = tt < nt && t < kend;
           if (MODE == MMode::kQkv) {
 #pragma unroll
             for (int bt = 0; bt < NBT; ++bt) {
@@ -316,7 +389,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
         if (lane < 16 && lvl == 0) ssq[wave][bt * kSeqTile + bp] = v;
       }
     }
-    if (si - c0 + 1 < a.sch && si + 1 < nstr) continue;
+    if (si - c0 + 1 < a.sch && si + 1 < nstr) return;
 
     // ---- epilogue of stripes c0 .. si -------------------------------------
     __syncthreads();
@@ -325,72 +398,80 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     // uniform count of rounds, stripes clamped into the chunk, sequences
     // past the batch and columns past the matrix clamped to real ones, so
     // every store is unconditional and duplicates store equal values)
-    constexpr int NCOL = 16;
     const int o = tid % NOUT;
-    const int bl = min(o / NCOL, nb - 1);
-    const int b = b0 + bl;
-    if ((MODE == MMode::kQkv || MODE == MMode::kGateUp) && c0 == 0) {
-      float t = 0.f;
-#pragma unroll
-      for (int w = 0; w < kMW; ++w) t += ssq[w][bl];
-      inv = 1.0f / sqrtf(t / (float)a.din + a.eps);
-    }
     const int rounds = (a.sch * NOUT + kMT - 1) / kMT;
-    for (int rd = 0; rd < rounds; ++rd) {
-      const int c = min((tid + rd * kMT) / NOUT, nch - 1);
-      const int s = blk + (c0 + c) * G;
-      const float* rc = red + (size_t)c * kMW * NOUT;
-      auto col = [&](int cc) {
+    if (MODE != MMode::kQkv && ks > 1) {
+      // this part's sums of the chunk's stripes, for the group's last block
+      for (int rd = 0; rd < rounds; ++rd) {
+        const int c = min((tid + rd * kMT) / NOUT, nch - 1);
+        const float* rc = red + (size_t)c * kMW * NOUT;
         float v = 0.f;
 #pragma unroll
-        for (int w = 0; w < kMW; ++w) v += rc[w * NOUT + bl * 16 + cc];
-        return v;
-      };
-      if (MODE == MMode::kGateUp) {
-        const int U = R / 2;  // units per stripe: gate columns [0, U), up columns [U, 2U)
-        const int nreal = min(U, a.rows - U * s);
-        const int n = min(o % NCOL, nreal - 1);
-        const int u = U * s + n;
-        const float gt = inv * col(n), up = inv * col(n + U);
-        const float av = gt / (1.0f + expf(-gt)) * up;
-        a.out[(size_t)b * a.rows + u] = av;
-        const uint32_t hi = bf16_bits(av);
-        const uint32_t lo = bf16_bits(av - __uint_as_float(hi << 16));
-        a.a_out[operand_offset(b, u, 0, a.a_out_nbtc)] = (uint16_t)hi;
-        a.a_out[operand_offset(b, u, 1, a.a_out_nbtc)] = (uint16_t)lo;
-      } else {
-        const int nreal = min(R, a.rows - R * s);
-        const int n = min(o % NCOL, nreal - 1);
-        const int row = R * s + n;
-        const size_t oi = (size_t)b * a.rows + row;
-        if (MODE == MMode::kQkv) {
-          a.out[oi] = inv * col(n);
-        } else if (MODE == MMode::kOproj) {
-          const float h1 = bf16_to_f32(a.x_bf16[oi]) + col(n);
-          a.out[oi] = h1;
-          // the gate/up operand: split of h1 * gamma2 at input `row`
-          const float hg = h1 * bf16_to_f32(a.gamma[row]);
-          const uint32_t hi = bf16_bits(hg);
-          const uint32_t lo = bf16_bits(hg - __uint_as_float(hi << 16));
-          a.a_out[operand_offset(b, row, 0, a.a_out_nbtc)] = (uint16_t)hi;
-          a.a_out[operand_offset(b, row, 1, a.a_out_nbtc)] = (uint16_t)lo;
-          // this stripe's sum of h1^2 per sequence (the 16 columns are one DPP row)
-          float sq = o % NCOL < nreal ? h1 * h1 : 0.f;
-          sq = row_stride4_sum(quad_sum(sq));
-          a.ssq_out[(size_t)s * a.batch + b] = sq;
-        } else {
-          a.out_bf16[oi] = f32_to_bf16(a.res_f32[oi] + col(n));
-        }
+        for (int w = 0; w < kMW; ++w) v += rc[w * NOUT + o];
+        st_c(kp_own + (size_t)(c0 + c) * NOUT + o, v);
+      }
+    } else {
+      if ((MODE == MMode::kQkv || MODE == MMode::kGateUp) && c0 == 0) inv = norm_factor();
+      const int bl = min(o / NCOL, nb - 1);
+      for (int rd = 0; rd < rounds; ++rd) {
+        const int c = min((tid + rd * kMT) / NOUT, nch - 1);
+        const float* rc = red + (size_t)c * kMW * NOUT + bl * NCOL;
+        finish(rg + (c0 + c) * NGr, o, [&](int cc) {
+          float v = 0.f;
+#pragma unroll
+          for (int w = 0; w < kMW; ++w) v += rc[w * NOUT + cc];
+          return v;
+        });
       }
     }
     __syncthreads();
     c0 = si + 1;
+  };
+  for (int si = 0; si < nstr; si += SPR) {
+    stripe(si, SlotBase<0>{});
+    if constexpr (SPR == 2) {
+      if (si + 1 < nstr) stripe(si + 1, SlotBase<RB>{});
+    }
+  }
+
+  // ---- split inputs: the group's last block sums the parts in order -------
+  if constexpr (MODE != MMode::kQkv) {
+    if (ks > 1) {
+      __shared__ int last_part;
+      wait_vm();  // this block's partial sums are stored
+      __syncthreads();
+      if (tid == 0) {
+        unsigned* tk = a.tickets + (size_t)blockIdx.y * NGr + rg;
+        const unsigned prev = __hip_atomic_fetch_add(tk, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool lst = prev == (unsigned)(ks - 1);
+        if (lst) st_cu(tk, 0u);  // ready for the next launch
+        last_part = lst;
+      }
+      __syncthreads();
+      if (!last_part) return;
+      if (MODE == MMode::kGateUp) inv = norm_factor();
+      const float* kp_grp = a.kpart + ((size_t)blockIdx.y * G + rg * ks) * a.kstride;
+      const int o = tid % NOUT;
+      const int bl = min(o / NCOL, nb - 1);
+      const int rounds = (nstr * NOUT + kMT - 1) / kMT;
+      for (int rd = 0; rd < rounds; ++rd) {
+        const int c = min((tid + rd * kMT) / NOUT, nstr - 1);
+        const float* pc = kp_grp + (size_t)c * NOUT + bl * NCOL;
+        finish(rg + c * NGr, o, [&](int cc) {
+          float v = 0.f;
+#pragma unroll
+          for (int q = 0; q < kMaxParts; ++q)
+            if (q < ks) v += ld_c(pc + (size_t)q * a.kstride + cc);
+          return v;
+        });
+      }
+    }
   }
 }
 
 template <MMode MODE, int NBT>
-hipError_t launch_nbt(const MfmaArgs& a, hipStream_t s, KernelEvents ev) {
-  dim3 grid(a.ns < kMGrid ? a.ns : kMGrid, (a.batch + kGroupSeq - 1) / kGroupSeq);
+hipError_t launch_nbt(const MfmaArgs& a, int ngr, hipStream_t s, KernelEvents ev) {
+  dim3 grid(ngr * a.ks, (a.batch + kGroupSeq - 1) / kGroupSeq);
   const size_t lds = (size_t)a.sch * kMW * NBT * kSeqTile * 16 * sizeof(float);
   const int nt = a.nt;
   // operands cached when the wave's run is short enough for its registers;
@@ -419,10 +500,51 @@ hipError_t launch_nbt(const MfmaArgs& a, hipStream_t s, KernelEvents ev) {
 }
 
 // stripes of the block whose partial sums share LDS before one epilogue
-inline int chunk_stripes(int ns, int nbt) {
-  const int per_block = (ns + kMGrid - 1) / kMGrid;
+inline int chunk_stripes(int per_block, int nbt) {
   const int cap = kMaxChunkBytes / (kMW * nbt * kSeqTile * 16 * (int)sizeof(float));
   return per_block < cap ? per_block : cap;
+}
+
+// Split inputs. Every block reads the whole activation operand of its k-tiles
+// (4 bytes per input and sequence, two bf16 levels: nbt KB per k-tile), and
+// a CU serves those loads in the same queue as its weight stream, so where
+// the operand outweighs a block's weights it costs more time than they do
+// (the down projection of the 16-sequence Phi-3 layer: 512 KB of operand
+// against 196 KB of weights per block). There the k-tiles are split into
+// kSplit parts: a row group of kSplit blocks takes the same stripes, each
+// block one part, so a block holds kSplit times the stripes and a kSplit-th
+// of the operand. Each block stores its partial sums (coherent stores), then
+// takes a ticket of its group; the last block of the group adds the partial
+// sums in part order and runs the epilogue, so the result does not depend on
+// which block comes last. The tickets and the last block's loads add about
+// 1.5 us, so the split is taken only where the operand is at least twice a
+// block's weights and 256 KB or more. Measured on MI355X (kernel us, split
+// into 4 against whole rows): 16-sequence Phi-3 down 19.1 -> 14.3 (taken);
+// its O projection (196 KB of operand) 8.4 -> 9.9 and gate/up (in 2 parts,
+// operand half the weights) 21.8 -> 22.9; GQA layer at 4 sequences (operand
+// equal to the weights) O 11.0 -> 10.2, down 21.6 -> 23.8.
+constexpr int kSplit = 4;
+constexpr int kSplitMinTiles = 128;     // k-tiles: 128 nbt KB of operand
+constexpr int kMinPartTiles = kMW / 2;  // k-tiles per part at least (half the waves busy)
+
+int nbt_of(int batch) { return batch > kSeqTile ? 2 : 1; }
+
+struct SplitGeom {
+  int ks, ngr, ktq, nt, nstr_max;
+};
+SplitGeom split_geom(MMode mode, int ns, int kt, int rh, int nbt) {
+  const int nstr0 = (ns + kMGrid - 1) / kMGrid;  // stripes per block, whole rows
+  // operand bytes (nbt KB per k-tile) >= 2 x weight bytes (rh x 64 B per k-tile and stripe)
+  const bool heavy = 16 * nbt >= 2 * nstr0 * rh && kt >= kSplitMinTiles;
+  int ks = mode != MMode::kQkv && heavy ? kSplit : 1;
+  while (ks > 1 && (kt < ks * kMinPartTiles || (ks - 1) * ((kt + ks - 1) / ks) >= kt)) ks /= 2;
+  SplitGeom g;
+  g.ks = ks;
+  g.ngr = ns < kMGrid / ks ? ns : kMGrid / ks;
+  g.ktq = (kt + ks - 1) / ks;
+  g.nt = (g.ktq + kMW - 1) / kMW;
+  g.nstr_max = (ns + g.ngr - 1) / g.ngr;
+  return g;
 }
 
 template <MMode MODE>
@@ -431,10 +553,25 @@ hipError_t launch_mmode(const MfmaArgs& a_in, hipStream_t s, KernelEvents ev) {
   if (a.batch < 1 || a.ns < 1 || a.kt < 1 || a.nt != (a.kt + kMW - 1) / kMW || a.din % 8 != 0) return hipErrorInvalidValue;
   if (a.rh < 2 || a.rh > 16 || a.rh % 2 != 0) return hipErrorInvalidValue;
   if (MODE == MMode::kGateUp && a.ns_in > kMaxStripesIn) return hipErrorInvalidValue;
-  const int nbt = a.batch > kSeqTile ? 2 : 1;
-  a.sch = chunk_stripes(a.ns, nbt);
-  if (nbt == 2) return launch_nbt<MODE, 2>(a, s, ev);
-  return launch_nbt<MODE, 1>(a, s, ev);
+  const int nbt = nbt_of(a.batch);
+  SplitGeom g = split_geom(MODE, a.ns, a.kt, a.rh, nbt);
+  const size_t nout = (size_t)nbt * kSeqTile * 16;
+  const size_t ny = (a.batch + kGroupSeq - 1) / kGroupSeq;
+  if (g.ks > 1 && (!a.kpart || !a.tickets || a.kpart_cap < ny * g.ngr * g.ks * g.nstr_max * nout ||
+                   a.tickets_cap < ny * g.ngr)) {
+    g.ks = 1;  // no scratch for the parts: whole rows per block
+    g.ngr = a.ns < kMGrid ? a.ns : kMGrid;
+    g.ktq = a.kt;
+    g.nt = a.nt;
+    g.nstr_max = (a.ns + g.ngr - 1) / g.ngr;
+  }
+  a.ks = g.ks;
+  a.ktq = g.ktq;
+  a.nt = g.nt;
+  a.kstride = (int)(g.nstr_max * nout);
+  a.sch = chunk_stripes(g.nstr_max, nbt);
+  if (nbt == 2) return launch_nbt<MODE, 2>(a, g.ngr, s, ev);
+  return launch_nbt<MODE, 1>(a, g.ngr, s, ev);
 }
 
 // Tiled copy of a row-major [rows, din] matrix (stride ld elements) in
@@ -466,6 +603,14 @@ __global__ __launch_bounds__(256) void tile_kernel(const uint16_t* __restrict__ 
 }
 
 }  // namespace
+
+void mfma_split_need(int mode, int ns, int kt, int rh, int batch, size_t* kpart_floats, size_t* tickets) {
+  const SplitGeom g = split_geom(static_cast<MMode>(mode), ns, kt, rh, nbt_of(batch));
+  const size_t ny = (batch + kGroupSeq - 1) / kGroupSeq;
+  const size_t nout = (size_t)nbt_of(batch) * kSeqTile * 16;
+  *kpart_floats = g.ks > 1 ? ny * g.ngr * g.ks * g.nstr_max * nout : 0;
+  *tickets = g.ks > 1 ? ny * g.ngr : 0;
+}
 
 hipError_t launch_mfma_qkv(const MfmaArgs& a, hipStream_t s, KernelEvents ev) {
   return launch_mmode<MMode::kQkv>(a, s, ev);

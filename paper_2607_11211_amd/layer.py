@@ -66,6 +66,13 @@ class WeightsDesc(ctypes.Structure):
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_11211_amd.build`")
+    # One HIP runtime per process: torch carries its own libamdhip64 under the
+    # same soname. Loaded first, it is the one this library binds to; loaded
+    # after a ROCm copy, it would be a second runtime that finds no device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     lib.fasttps_layer_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]

@@ -56,6 +56,21 @@ SHAPES = [
     # d = 128, GQA 4, long RoPE base, intermediate not a multiple of 8 units per stripe boundary
     LayerConfig(name="m_gqa128_b4", index=54, batch=4, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
                 intermediate=2824, rope_base=500000.0, max_seq=1100, pos=(5, 511, 1000, 640)),
+    # split inputs (operand at least twice a block's weights, 128+ k-tiles): the down projection's
+    # 131 k-tiles in 4 parts of 33 (the last 32), one stripe of 16 rows per row group
+    LayerConfig(name="m_split_down_b16", index=58, batch=16, hidden=512, n_heads=8, n_kv_heads=2, head_dim=64,
+                intermediate=4192, rope_base=10000.0, max_seq=200, pos=tuple((29 * i + 7) % 199 for i in range(16))),
+    # split down projection over 33 stripes of 8 rows (hidden 264) and two grid rows (20 sequences)
+    LayerConfig(name="m_split_down_b20", index=59, batch=20, hidden=264, n_heads=4, n_kv_heads=4, head_dim=64,
+                intermediate=4096, rope_base=10000.0, max_seq=120, pos=tuple((13 * i) % 117 for i in range(20))),
+    # split O projection (32 x 128 = 4096 inputs, 16 stripes): its last block writes h1, the gate/up
+    # operand and the sums of h1^2
+    LayerConfig(name="m_split_o_b12", index=60, batch=12, hidden=256, n_heads=32, n_kv_heads=8, head_dim=128,
+                intermediate=688, rope_base=10000.0, max_seq=100, pos=tuple(range(3, 99, 8))),
+    # split gate/up projection (4096 inputs, 32 stripes of 8 gate + 8 up rows): RMSNorm2 and SiLU * up
+    # in the last block
+    LayerConfig(name="m_split_gu_b16", index=61, batch=16, hidden=4096, n_heads=4, n_kv_heads=4, head_dim=64,
+                intermediate=256, rope_base=10000.0, max_seq=64, pos=tuple(range(0, 64, 4))),
 ]
 
 
@@ -146,3 +161,41 @@ def test_path_hook_errors():
     W1.free()
     one.destroy()
     two.destroy()
+
+
+def test_split_graph_replays_equal_eager():
+    """The split projections' tickets are left at zero by every launch: graph
+    replays and eager steps in between give the first eager step's bits."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    cfg = next(c for c in SHAPES if c.name == "m_split_down_b16")
+    inp = inputs.make_layer_inputs(cfg)
+    lay = L.Layer(cfg)
+    lay.set_gemm_path(L.GEMM_MATRIX)
+    W = lay.pack({k: L.to_device(v) for k, v in inp.weights.items()})
+    x = L.to_device(inp.x)
+    kc, vc = L.to_device(inp.k_cache), L.to_device(inp.v_cache)
+    y = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+    lay.step(W, x, inp.pos, kc, vc, y, stream)
+    torch.cuda.synchronize()
+    y_eager = L.from_device(y)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(stream)
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            lay.step(W, x, inp.pos, kc, vc, y, s)
+    stream.wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        y.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(L.from_device(y), y_eager), f"replay {rep} differs from the eager step"
+        lay.step(W, x, inp.pos, kc, vc, y, stream)
+        torch.cuda.synchronize()
+        assert np.array_equal(L.from_device(y), y_eager)
+    del g
+    W.free()
+    lay.destroy()
