@@ -43,8 +43,13 @@
 // double precision, before it is stored and used.
 // A second small kernel combines the splits of each (b, head) with the
 // log-sum-exp identity (one wave per (b, head) up to 32 splits, a block
-// beyond). (Cross-block tickets are avoided on purpose: on this
-// chip an agent-scope fence per block costs far more than a kernel boundary.)
+// beyond). A merge inside the split launch (each block stores its state
+// with coherent stores, waits for them and takes a ticket of its (sequence,
+// KV head); the last one merges) was measured slower on MI355X: the store
+// acknowledgements and the ticket's round trip under full HBM load hold
+// every block longer than the merge launch costs (Phi-3 layer at KV 4096:
+// attention 12.0 -> 16.0 us against a 4.4 us merge kernel, 59.9 -> 61.7 us
+// per layer; 16-sequence ragged batch: attention 75.9 -> 87.2 us).
 #include "attn_body.h"
 
 namespace fasttps {
