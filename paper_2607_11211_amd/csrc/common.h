@@ -121,6 +121,14 @@ __device__ __forceinline__ float dpp_mov(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 
+// 16 bytes of the neighbouring lane (lane ^ 1)
+__device__ __forceinline__ v4u dpp_swap_pair(v4u v) {
+  return v4u{(unsigned)__builtin_amdgcn_mov_dpp((int)v.x, kDppQuadXor1, 0xF, 0xF, false),
+             (unsigned)__builtin_amdgcn_mov_dpp((int)v.y, kDppQuadXor1, 0xF, 0xF, false),
+             (unsigned)__builtin_amdgcn_mov_dpp((int)v.z, kDppQuadXor1, 0xF, 0xF, false),
+             (unsigned)__builtin_amdgcn_mov_dpp((int)v.w, kDppQuadXor1, 0xF, 0xF, false)};
+}
+
 // Sum over the 4 lanes of a quad; every lane gets the result.
 __device__ __forceinline__ float quad_sum(float v) {
   v += dpp_mov<kDppQuadXor1>(v);

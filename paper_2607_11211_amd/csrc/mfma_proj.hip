@@ -187,10 +187,14 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     const int b = b0 + min(bt * kSeqTile + bp, nb - 1);
     return *reinterpret_cast<const v4u*>(a.x_bf16 + (size_t)b * a.din + k0);
   };
-  auto g_chunk = [&](int t) {  // from the LDS copy
+  auto g_chunk = [&](int t) {  // from the LDS copy (this wave's entries)
     const int k0 = min(32 * min(t, a.kt - 1) + 8 * kg, a.din - 8);
     return gam[k0 / 8];
   };
+  // QKV with two batch tiles: the two level lanes of a (sequence slot,
+  // k-group) need the same x chunks, so lane level l loads batch tile l's and
+  // the pair swaps them (one load per k-tile instead of two)
+  constexpr bool XPAIR = MODE == MMode::kQkv && CACHED && NBT == 2 && NT <= 6;  // (runs of 8 tiles: spills)
   auto ready_chunk = [&](int t, int bt) {
     return reinterpret_cast<const v4u*>(a.a_in)[((size_t)min(t, a.kt - 1) * a.nbtc + btg0 + bt) * kWave + op_lane(bt)];
   };
@@ -201,15 +205,25 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
 
   // ---- loads issued ahead of the weight stream: gamma1 (QKV), the cached
   // operands (or the x chunks they are built from)
+  // QKV: each wave stages the gamma1 chunks of its own k-tiles (lane 4 tt +
+  // k-group; a run has at most 16 tiles), so no block barrier waits for the
+  // other waves' loads; lanes past the run write a neighbour's entries with
+  // the values it writes itself
+  const int gk8 = min(32 * min(tbase + lane / 4, a.kt - 1) + 8 * (lane & 3), a.din - 8) / 8;
   v4u gload = {0u, 0u, 0u, 0u};
-  if (MODE == MMode::kQkv) gload = reinterpret_cast<const v4u*>(a.gamma)[min(tid, a.din / 8 - 1)];
+  if (MODE == MMode::kQkv) gload = reinterpret_cast<const v4u*>(a.gamma)[gk8];
   v4u acache[CACHED ? NT : 1][NBT];
   if constexpr (CACHED) {
 #pragma unroll
-    for (int tt = 0; tt < NT; ++tt)
+    for (int tt = 0; tt < NT; ++tt) {
+      if constexpr (XPAIR) {
+        acache[tt][0] = x_chunk(tbase + tt, lvl);
+      } else {
 #pragma unroll
-      for (int bt = 0; bt < NBT; ++bt)
-        acache[tt][bt] = MODE == MMode::kQkv ? x_chunk(tbase + tt, bt) : ready_chunk(tbase + tt, bt);
+        for (int bt = 0; bt < NBT; ++bt)
+          acache[tt][bt] = MODE == MMode::kQkv ? x_chunk(tbase + tt, bt) : ready_chunk(tbase + tt, bt);
+      }
+    }
   }
   __builtin_amdgcn_sched_barrier(0);
 
@@ -238,11 +252,9 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     load_item(r, r);
     __builtin_amdgcn_sched_barrier(0);
   }
-  if (MODE == MMode::kQkv) {
-    // gamma1 into LDS (its load is the oldest, so this waits for it only)
-    if (tid < a.din / 8) gam[tid] = gload;
-    __syncthreads();
-  }
+  // gamma1 into LDS (its load is the oldest, so this waits for it only);
+  // read back by this wave only, so no barrier
+  if (MODE == MMode::kQkv) gam[gk8] = gload;
   // the cached operands, once their loads (older than the ring's) are in;
   // the QKV operands are built from their x chunks during the first stripe
   // instead, each just before its first MFMA, where the conversion overlaps
@@ -333,6 +345,13 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
         const int tt = tt0 + rr;
         bf16x8 A[NBT];
         if constexpr (CACHED) {
+          if constexpr (XPAIR) {
+            if (si == 0) {
+              const v4u own = acache[tt][0], other = dpp_swap_pair(own);
+              acache[tt][1] = lvl ? own : other;
+              acache[tt][0] = lvl ? other : own;
+            }
+          }
 #pragma unroll
           for (int bt = 0; bt < NBT; ++bt) {
             if (MODE == MMode::kQkv && si == 0) {
@@ -551,6 +570,7 @@ template <MMode MODE>
 hipError_t launch_mmode(const MfmaArgs& a_in, hipStream_t s, KernelEvents ev) {
   MfmaArgs a = a_in;
   if (a.batch < 1 || a.ns < 1 || a.kt < 1 || a.nt != (a.kt + kMW - 1) / kMW || a.din % 8 != 0) return hipErrorInvalidValue;
+  if (MODE == MMode::kQkv && a.din > kMaxHidden) return hipErrorInvalidValue;  // gamma1 in LDS, 16 tiles per wave
   if (a.rh < 2 || a.rh > 16 || a.rh % 2 != 0) return hipErrorInvalidValue;
   if (MODE == MMode::kGateUp && a.ns_in > kMaxStripesIn) return hipErrorInvalidValue;
   const int nbt = nbt_of(a.batch);
