@@ -225,6 +225,33 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
                                  with FASTTPS_ERR_UNSUPPORTED before any launch */
 FASTTPS_API int fasttps_set_gemm_path(fasttps_layer* layer, int32_t path);
 
+/* How fasttps_weights_pack stores the four projections for a layer with
+ * max_batch > 1 (a layer with max_batch == 1 stores them row-major only).
+ *   FASTTPS_WEIGHTS_ROWS_AND_TILES
+ *                        (default) row-major for the vector path and in the
+ *                        MFMA tile order for the matrix path: twice the
+ *                        projection memory (Phi-3-mini: 453 instead of 227 MB
+ *                        per layer), so that steps of one sequence keep the
+ *                        vector kernels, the faster ones at batch 1 (Phi-3
+ *                        layer at KV 4096 on MI355X: 59.9 against 68.0 us per
+ *                        layer step on the matrix path)
+ *   FASTTPS_WEIGHTS_TILES
+ *                        the tile order only: every step with these weights
+ *                        runs the matrix path, also at one sequence; steps
+ *                        that need row-major weights (FASTTPS_GEMM_VECTOR or
+ *                        FASTTPS_GEMM_FUSED set, FASTTPS_MLP_FUSED set,
+ *                        fasttps_decode_step_noalloc,
+ *                        fasttps_decode_step_unfused) fail with
+ *                        FASTTPS_ERR_INVALID_ARG before any launch, and so
+ *                        does a pack with FASTTPS_MLP_FUSED selected.
+ * Applies to weights packed afterwards with this handle (the pack then
+ * allocates and frees a temporary row-major copy of W_q|W_k|W_v). Returns
+ * FASTTPS_ERR_INVALID_ARG for an unknown layout, or for FASTTPS_WEIGHTS_TILES
+ * on a layer with max_batch == 1. */
+#define FASTTPS_WEIGHTS_ROWS_AND_TILES 0
+#define FASTTPS_WEIGHTS_TILES 1
+FASTTPS_API int fasttps_set_weight_layout(fasttps_layer* layer, int32_t layout);
+
 /* How the MLP (RMSNorm2, gate/up, siLu_Mul, down, residual) runs.
  *   FASTTPS_MLP_SPLIT  (default) two kernels: gate/up with siLu_Mul stores
  *                      h^sm (fp32, K values per sequence), the down

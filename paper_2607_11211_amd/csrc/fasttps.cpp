@@ -187,6 +187,7 @@ struct fasttps_layer {
   // the MLP as one kernel with h^sm on chip (fasttps_set_mlp_path): its
   // partial sums of y [slices][max_batch][D], allocated when first selected
   int mlp_path = FASTTPS_MLP_SPLIT;
+  int weight_layout = FASTTPS_WEIGHTS_ROWS_AND_TILES;  // how later packs store the projections
   float* mlp_part = nullptr;
   bool mlp_a_written = false;  // the last step stored h^sm (FASTTPS_DBG_MLP_A)
   // the fused kernel's phase hand-over: per-block phase flags, the epoch of
@@ -529,10 +530,14 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   const size_t q = (size_t)c.n_heads * d, kv = (size_t)c.n_kv_heads * d;
   const size_t n_qkv = (q + 2 * kv) * D, n_o = D * q, n_gu = 2 * K * D, n_d = K * D;
   const bool tiled = c.max_batch > 1;
+  const bool rows = !tiled || l->weight_layout == FASTTPS_WEIGHTS_ROWS_AND_TILES;  // row-major copies
   const LayerTiles lt = layer_tiles(c);
   const bool slices = l->mlp_path == FASTTPS_MLP_FUSED;
+  if (slices && !rows)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the fused MLP needs row-major weights (layout FASTTPS_WEIGHTS_TILES set)");
   const size_t n_sl = (size_t)mlp_fused_blocks((int)K) * D * mlp_fused_u8((int)K);
-  size_t offs[11], sizes[11] = {n_qkv * 2, n_o * 2, n_gu * 2, n_d * 2, D * 2, D * 2,
+  size_t offs[11], sizes[11] = {rows ? n_qkv * 2 : 0, rows ? n_o * 2 : 0, rows ? n_gu * 2 : 0, rows ? n_d * 2 : 0,
+                                D * 2, D * 2,
                                 tiled ? lt.qkv.elems() * 2 : 0, tiled ? lt.o.elems() * 2 : 0,
                                 tiled ? lt.gu.elems() * 2 : 0, tiled ? lt.down.elems() * 2 : 0,
                                 slices ? n_sl * 2 : 0};
@@ -554,10 +559,12 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   pw->magic = kWeightsMagic;
   pw->cfg = c;
   pw->arena = arena;
-  pw->w_qkv = reinterpret_cast<uint16_t*>(base + offs[0]);
-  pw->w_o = reinterpret_cast<uint16_t*>(base + offs[1]);
-  pw->w_gu = reinterpret_cast<uint16_t*>(base + offs[2]);
-  pw->w_down = reinterpret_cast<uint16_t*>(base + offs[3]);
+  if (rows) {
+    pw->w_qkv = reinterpret_cast<uint16_t*>(base + offs[0]);
+    pw->w_o = reinterpret_cast<uint16_t*>(base + offs[1]);
+    pw->w_gu = reinterpret_cast<uint16_t*>(base + offs[2]);
+    pw->w_down = reinterpret_cast<uint16_t*>(base + offs[3]);
+  }
   pw->attn_norm = reinterpret_cast<uint16_t*>(base + offs[4]);
   pw->mlp_norm = reinterpret_cast<uint16_t*>(base + offs[5]);
   if (tiled) {
@@ -570,29 +577,49 @@ int fasttps_weights_pack(fasttps_layer* l, const fasttps_weights_desc* w, void* 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const auto* g = static_cast<const uint16_t*>(w->w_gate);
   const auto* u = static_cast<const uint16_t*>(w->w_up);
-  if ((e = hipMemcpyAsync(pw->w_qkv, w->w_q, q * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(pw->w_qkv + q * D, w->w_k, kv * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(pw->w_qkv + (q + kv) * D, w->w_v, kv * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(pw->w_o, w->w_o, n_o * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+  // the tile order only: the tiles come from the caller's matrices, W_q|W_k|W_v
+  // through a temporary row-major copy (freed before returning)
+  void* qkv_tmp = nullptr;
+  if (!rows && (e = hipMalloc(&qkv_tmp, n_qkv * 2)) != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(arena);
+    pw->magic = kDeadMagic;
+    delete pw;
+    return fail(FASTTPS_ERR_OOM, "hipMalloc(%zu): %s", n_qkv * 2, hipGetErrorString(e));
+  }
+  uint16_t* qkv_rows = rows ? pw->w_qkv : static_cast<uint16_t*>(qkv_tmp);
+  const uint16_t* o_rows = rows ? pw->w_o : static_cast<const uint16_t*>(w->w_o);
+  const uint16_t* down_rows = rows ? pw->w_down : static_cast<const uint16_t*>(w->w_down);
+  if ((e = hipMemcpyAsync(qkv_rows, w->w_q, q * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(qkv_rows + q * D, w->w_k, kv * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(qkv_rows + (q + kv) * D, w->w_v, kv * D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (rows && (e = hipMemcpyAsync(pw->w_o, w->w_o, n_o * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
       (e = hipMemcpyAsync(pw->attn_norm, w->attn_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
       (e = hipMemcpyAsync(pw->mlp_norm, w->mlp_norm, D * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
-      (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, kInterlaceTile, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(pw->w_down, w->w_down, n_d * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (rows && (e = launch_interlace_gate_up(g, u, pw->w_gu, (int)K, (int)D, kInterlaceTile, s)) != hipSuccess) ||
+      (rows && (e = hipMemcpyAsync(pw->w_down, w->w_down, n_d * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess) ||
       (slices && (e = launch_pack_down_slices(pw->w_down, pw->w_down_slices, (int)D, (int)K, s)) != hipSuccess) ||
-      (tiled && ((e = launch_tile_weights(pw->w_qkv, nullptr, (int)(q + 2 * kv), (int)D, (int)D, lt.qkv.ns,
+      (tiled && ((e = launch_tile_weights(qkv_rows, nullptr, (int)(q + 2 * kv), (int)D, (int)D, lt.qkv.ns,
                                           lt.qkv.kt, lt.qkv.rh, pw->t_qkv, s)) != hipSuccess ||
-                 (e = launch_tile_weights(pw->w_o, nullptr, (int)D, (int)q, (int)q, lt.o.ns, lt.o.kt, lt.o.rh,
+                 (e = launch_tile_weights(o_rows, nullptr, (int)D, (int)q, (int)q, lt.o.ns, lt.o.kt, lt.o.rh,
                                           pw->t_o, s)) != hipSuccess ||
                  (e = launch_tile_weights(g, u, (int)K, (int)D, (int)D, lt.gu.ns, lt.gu.kt, lt.gu.rh, pw->t_gu, s)) !=
                      hipSuccess ||
-                 (e = launch_tile_weights(pw->w_down, nullptr, (int)D, (int)K, (int)K, lt.down.ns, lt.down.kt,
+                 (e = launch_tile_weights(down_rows, nullptr, (int)D, (int)K, (int)K, lt.down.ns, lt.down.kt,
                                           lt.down.rh, pw->t_down, s)) != hipSuccess)) ||
       (e = hipStreamSynchronize(s)) != hipSuccess) {
     (void)hipStreamSynchronize(s);
+    if (qkv_tmp) (void)hipFree(qkv_tmp);
     (void)hipFree(arena);
     pw->magic = kDeadMagic;
     delete pw;
     return hip_fail(e, "weight packing");
+  }
+  if (qkv_tmp && (e = hipFree(qkv_tmp)) != hipSuccess) {
+    (void)hipFree(arena);
+    pw->magic = kDeadMagic;
+    delete pw;
+    return hip_fail(e, "hipFree of the packing copy");
   }
   track(g_weights, pw, true);
   *out = pw;
@@ -738,8 +765,14 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   const bool mlp_fused = !S.noalloc && l->mlp_path == FASTTPS_MLP_FUSED;
   if (mlp_fused && !w->w_down_slices)
     return fail(FASTTPS_ERR_INVALID_ARG, "the fused MLP needs weights packed while it was selected on the layer");
+  // weights in the tile order only run the matrix path, at any batch
+  const bool tiles_only = w->w_qkv == nullptr;
+  if (tiles_only && (S.noalloc || mlp_fused || l->gemm_path == FASTTPS_GEMM_VECTOR ||
+                     l->gemm_path == FASTTPS_GEMM_FUSED))
+    return fail(FASTTPS_ERR_INVALID_ARG,
+                "weights packed in the tile order only (FASTTPS_WEIGHTS_TILES) run the matrix path only");
   const bool mfma = !S.noalloc && !mlp_fused &&
-                    (l->gemm_path == FASTTPS_GEMM_MATRIX ||
+                    (l->gemm_path == FASTTPS_GEMM_MATRIX || tiles_only ||
                      (l->gemm_path == FASTTPS_GEMM_AUTO && have_tiles && batch >= kMfmaMinBatch));
   if (mfma && !have_tiles)
     return fail(FASTTPS_ERR_INVALID_ARG, "the matrix-core path needs a layer and weights with max_batch > 1");
@@ -1108,6 +1141,8 @@ int fasttps_decode_step_unfused(fasttps_layer* l, const fasttps_weights* w, cons
   const int st = check_step(l, w, x, pos, batch, k_cache, v_cache, y, &maxp);
   if (st) return st;
   if (!l->uf_arena) return fail(FASTTPS_ERR_INVALID_ARG, "call fasttps_unfused_enable on this layer first");
+  if (!w->w_qkv)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the op-by-op baseline needs row-major weights (FASTTPS_WEIGHTS_TILES set)");
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -1138,6 +1173,17 @@ int fasttps_decode_step_unfused(fasttps_layer* l, const fasttps_weights* w, cons
   u.eps = c.rms_eps;
   for (int b = 0; b < batch; ++b) u.pos.p[b] = pos[b];
   if ((e = launch_unfused(u, static_cast<hipStream_t>(stream))) != hipSuccess) return hip_fail(e, "unfused launch");
+  return FASTTPS_OK;
+}
+
+int fasttps_set_weight_layout(fasttps_layer* l, int32_t layout) {
+  g_last_error.clear();
+  if (!layer_ok(l)) return fail(FASTTPS_ERR_BAD_HANDLE, "bad layer handle");
+  if (layout != FASTTPS_WEIGHTS_ROWS_AND_TILES && layout != FASTTPS_WEIGHTS_TILES)
+    return fail(FASTTPS_ERR_INVALID_ARG, "unknown weight layout %d", layout);
+  if (layout == FASTTPS_WEIGHTS_TILES && !l->op_o)
+    return fail(FASTTPS_ERR_INVALID_ARG, "the tile order only needs a layer with max_batch > 1");
+  l->weight_layout = layout;
   return FASTTPS_OK;
 }
 

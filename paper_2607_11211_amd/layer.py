@@ -30,6 +30,7 @@ DBG_QK_ROPE, DBG_H, DBG_H2 = 5, 6, 7
 
 GEMM_AUTO, GEMM_VECTOR, GEMM_MATRIX, GEMM_FUSED = 0, 1, 2, 3
 MLP_SPLIT, MLP_FUSED = 0, 1
+WEIGHTS_ROWS_AND_TILES, WEIGHTS_TILES = 0, 1
 
 KV_FP8_E4M3 = 1
 KV_INT8 = 2
@@ -39,7 +40,7 @@ EXPORTS = ("fasttps_layer_create", "fasttps_weights_pack", "fasttps_decode_step"
            "fasttps_profile_begin", "fasttps_profile_end", "fasttps_kernel_name",
            "fasttps_unfused_enable", "fasttps_decode_step_unfused", "fasttps_set_attention_p_bf16",
            "fasttps_decode_step_kv8", "fasttps_set_gemm_path", "fasttps_set_debug", "fasttps_validate_step",
-           "fasttps_set_mlp_path", "fasttps_decode_step_noalloc",
+           "fasttps_set_mlp_path", "fasttps_decode_step_noalloc", "fasttps_set_weight_layout",
            "fasttps_weights_free", "fasttps_layer_destroy", "fasttps_status_string", "fasttps_last_error")
 NUM_KERNELS = 7
 
@@ -87,6 +88,7 @@ def _load() -> ctypes.CDLL:
     lib.fasttps_set_gemm_path.argtypes = [vp, i32]
     lib.fasttps_set_debug.argtypes = [vp, i32]
     lib.fasttps_set_mlp_path.argtypes = [vp, i32]
+    lib.fasttps_set_weight_layout.argtypes = [vp, i32]
     lib.fasttps_validate_step.argtypes = [ctypes.POINTER(Config), vp, ctypes.POINTER(i32), i32, vp, vp, vp, i32]
     lib.fasttps_debug_read.argtypes = [vp, i32, i32, vp, sz, vp]
     lib.fasttps_profile_begin.argtypes = [vp, i32]
@@ -104,7 +106,7 @@ def _load() -> ctypes.CDLL:
                  "fasttps_layer_destroy", "fasttps_unfused_enable", "fasttps_decode_step_unfused",
                  "fasttps_set_attention_p_bf16", "fasttps_decode_step_kv8", "fasttps_set_gemm_path",
                  "fasttps_set_debug", "fasttps_validate_step", "fasttps_decode_step_noalloc",
-                 "fasttps_set_mlp_path"):
+                 "fasttps_set_mlp_path", "fasttps_set_weight_layout"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -276,6 +278,11 @@ class Layer:
         """MLP_SPLIT (gate/up stores h^sm, down reads it) or MLP_FUSED (h^sm kept on chip;
         weights must be packed after selecting it)."""
         _check(LIB.fasttps_set_mlp_path(self.handle, int(path)), "fasttps_set_mlp_path")
+
+    def set_weight_layout(self, layout: int) -> None:
+        """WEIGHTS_ROWS_AND_TILES (default) or WEIGHTS_TILES (the MFMA tile order only; every
+        step with such weights runs the matrix path); applies to weights packed afterwards."""
+        _check(LIB.fasttps_set_weight_layout(self.handle, int(layout)), "fasttps_set_weight_layout")
 
     def set_debug(self, enable: bool) -> None:
         """Test hook: later steps also write q, k after RoPE and the two normalized activations."""

@@ -199,3 +199,70 @@ def test_split_graph_replays_equal_eager():
     del g
     W.free()
     lay.destroy()
+
+
+def test_tiles_only_layout():
+    """Weights packed in the MFMA tile order only: steps of one and three
+    sequences run the matrix path, meet the oracle's bars and give the bits of
+    the matrix path over weights that carry both layouts; steps that need the
+    row-major weights are refused before any launch."""
+    import torch
+    from paper_2607_11211_amd import layer as L
+    big = LayerConfig(name="m_tiles", index=62, batch=3, hidden=512, n_heads=8, n_kv_heads=2, head_dim=64,
+                      intermediate=1376, rope_base=10000.0, max_seq=160, pos=(5, 77, 150))
+    inp = inputs.make_layer_inputs(big)
+    dev_w = {k: L.to_device(v) for k, v in inp.weights.items()}
+    both = L.Layer(big, max_batch=4)
+    both.set_gemm_path(L.GEMM_MATRIX)
+    Wb = both.pack(dev_w)
+    tl = L.Layer(big, max_batch=4)
+    tl.set_weight_layout(L.WEIGHTS_TILES)
+    Wt = tl.pack(dev_w)
+    Wf = ref.widen_weights(inp.weights)
+    for nb in (1, 3):
+        cfg = LayerConfig(name=f"m_tiles{nb}", index=62, batch=nb, hidden=512, n_heads=8, n_kv_heads=2,
+                          head_dim=64, intermediate=1376, rope_base=10000.0, max_seq=160, pos=big.pos[:nb])
+        step_inp = inputs.LayerInputs(cfg=cfg, x=inp.x[:nb].copy(), pos=inp.pos[:nb].copy(), weights=inp.weights,
+                                      k_cache=inp.k_cache[:nb].copy(), v_cache=inp.v_cache[:nb].copy())
+        r = ref.decode_layer_cfg(cfg, step_inp.x, step_inp.pos, step_inp.k_cache, step_inp.v_cache, Wf)
+        log(f"tiles-only step of {nb}")
+        gt = run_gpu(cfg, step_inp, layer=tl, weights=Wt)
+        full_check(cfg, step_inp, gt, r)
+        gb = run_gpu(cfg, step_inp, layer=both, weights=Wb)
+        assert np.array_equal(gt["y"], gb["y"])
+    # steps that need the row-major weights
+    x = L.to_device(inp.x)
+    kc, vc = L.to_device(inp.k_cache), L.to_device(inp.v_cache)
+    y = torch.zeros_like(x)
+    for path in (L.GEMM_VECTOR, L.GEMM_FUSED):
+        tl.set_gemm_path(path)
+        with pytest.raises(L.FastTPSError) as e:
+            tl.step(Wt, x, inp.pos, kc, vc, y)
+        assert e.value.status == L.ERR_INVALID_ARG
+    tl.set_gemm_path(L.GEMM_AUTO)
+    with pytest.raises(L.FastTPSError) as e:
+        tl.step_noalloc(Wt, x, inp.pos, kc, vc, y)
+    assert e.value.status == L.ERR_INVALID_ARG
+    tl.enable_unfused()
+    with pytest.raises(L.FastTPSError) as e:
+        tl.step_unfused(Wt, x, inp.pos, kc, vc, y)
+    assert e.value.status == L.ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert not L.from_device(y).any()
+    assert np.array_equal(L.from_device(kc), inp.k_cache) and np.array_equal(L.from_device(vc), inp.v_cache)
+    # the fused MLP needs row-major W_down; the layout needs max_batch > 1
+    tl.set_mlp_path(L.MLP_FUSED)
+    with pytest.raises(L.FastTPSError) as e:
+        tl.pack(dev_w)
+    assert e.value.status == L.ERR_INVALID_ARG
+    one = L.Layer(big, max_batch=1)
+    with pytest.raises(L.FastTPSError) as e:
+        one.set_weight_layout(L.WEIGHTS_TILES)
+    assert e.value.status == L.ERR_INVALID_ARG
+    with pytest.raises(L.FastTPSError) as e:
+        one.set_weight_layout(7)
+    assert e.value.status == L.ERR_INVALID_ARG
+    for W in (Wb, Wt):
+        W.free()
+    for lay in (both, tl, one):
+        lay.destroy()
