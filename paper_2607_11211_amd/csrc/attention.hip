@@ -236,7 +236,12 @@ hipError_t launch_dg(const AttnArgs& a, hipStream_t s, KernelEvents ev) {
   // tiles in flight per lane: a tile is D / 8 registers of K and V; the
   // query quarter and the softmax state take (D / 4 + 2) G more. Two for one
   // or two query heads (103-226 VGPRs at d = 64-128: at least the two blocks
-  // per CU the split targets), one for groups of four (up to 256 VGPRs)
+  // per CU the split targets), one for groups of four (up to 256 VGPRs).
+  // A group of four as two blocks of two heads each (two tiles in flight,
+  // the pair reading the same K/V tiles at about the same time) was measured
+  // slower on MI355X: GQA layer at 4 x 32768, attention 96.2 -> 116.8 us
+  // (plain loads) and 124.3 us (whole-line non-temporal loads); the pair's
+  // second reads do not come from cache often enough.
   constexpr int NRING = G <= 2 ? 2 : 1;
   dim3 grid(a.nsplit, a.n_kv_heads, a.batch);
   int maxp = 0;
