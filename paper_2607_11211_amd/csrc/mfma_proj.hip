@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     }
   };
   // split inputs: this block's partial sums [stripe][slot]
-  float* kp_own = a.kpart + ((size_t)blockIdx.y * G + blk) * a.kstride;
+  float* kp_own = ks > 1 ? a.kpart + ((size_t)blockIdx.y * G + blk) * a.kstride : nullptr;
   // stripe si, whose items use ring slots SB .. SB + RB - 1 (SB: a constant)
   auto stripe = [&](int si, auto sb) {
     constexpr int SB = decltype(sb)::value;
