@@ -203,7 +203,8 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
  *                        activations split into two bf16 levels, fp32
  *                        accumulation); needs max_batch > 1, for which
  *                        fasttps_weights_pack also stores the weights in the
- *                        MFMA tile order (about twice the weight memory)
+ *                        MFMA tile order (about twice the weight memory, or
+ *                        the tiles only: fasttps_set_weight_layout)
  *   FASTTPS_GEMM_FUSED   one sequence in one persistent kernel (below); a
  *                        measured alternative, slower on MI355X than the six
  *                        kernels of the vector path replayed from a HIP graph

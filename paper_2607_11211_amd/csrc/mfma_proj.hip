@@ -36,6 +36,9 @@
 //   * Blocks take the stripes round-robin; the 16 waves of a block split
 //     the k-tiles of a stripe into 16 contiguous runs (nt tiles each, the
 //     last runs padded), so a stripe's partial sums meet once, in LDS.
+//   * Where the operand outweighs a block's weights, row groups of blocks
+//     split the k-tiles instead and the last block of a group adds the
+//     parts (split inputs, below).
 //   * Each wave keeps NBUF tiles in flight (with their activation operands).
 //     Every global load and store is issued unconditionally (clamped
 //     addresses, duplicate stores of equal values), so the number of memory
