@@ -266,3 +266,31 @@ def test_tiles_only_layout():
         W.free()
     for lay in (both, tl, one):
         lay.destroy()
+
+
+def test_split_and_whole_rows_on_one_handle():
+    """Steps of 16 sequences (down projection split across blocks), then 3
+    (one batch tile: whole rows), then 16 again on one handle: each checked
+    against the oracle, the last with the first step's bits."""
+    from paper_2607_11211_amd import layer as L
+    big = next(c for c in SHAPES if c.name == "m_split_down_b16")
+    inp = inputs.make_layer_inputs(big)
+    lay = L.Layer(big)
+    lay.set_gemm_path(L.GEMM_MATRIX)
+    W = lay.pack({k: L.to_device(v) for k, v in inp.weights.items()})
+    Wf = ref.widen_weights(inp.weights)
+    ys = []
+    for nb in (16, 3, 16):
+        cfg = LayerConfig(name=f"m_split_mix{nb}", index=58, batch=nb, hidden=big.hidden, n_heads=big.n_heads,
+                          n_kv_heads=big.n_kv_heads, head_dim=big.head_dim, intermediate=big.intermediate,
+                          rope_base=big.rope_base, max_seq=big.max_seq, pos=big.pos[:nb])
+        step_inp = inputs.LayerInputs(cfg=cfg, x=inp.x[:nb].copy(), pos=inp.pos[:nb].copy(), weights=inp.weights,
+                                      k_cache=inp.k_cache[:nb].copy(), v_cache=inp.v_cache[:nb].copy())
+        r = ref.decode_layer_cfg(cfg, step_inp.x, step_inp.pos, step_inp.k_cache, step_inp.v_cache, Wf)
+        log(f"split/whole-rows step of {nb}")
+        gpu = run_gpu(cfg, step_inp, layer=lay, weights=W)
+        full_check(cfg, step_inp, gpu, r)
+        ys.append(gpu["y"])
+    assert np.array_equal(ys[0], ys[2])
+    W.free()
+    lay.destroy()
