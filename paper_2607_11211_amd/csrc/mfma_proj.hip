@@ -69,11 +69,6 @@ constexpr int kMaxParts = 4;               // input parts of a split projection
 
 enum class MMode { kQkv, kOproj, kGateUp, kDown };
 
-template <int V>
-struct SlotBase {
-  static constexpr int value = V;
-};
-
 __device__ __forceinline__ bf16x8 as_bf16x8(v4u v) { return __builtin_bit_cast(bf16x8, v); }
 
 // bf16 bits of a float, nearest even, as selects (no branches in the
@@ -117,11 +112,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   constexpr bool CACHED = NT > 0;
   constexpr int NOUT = NBT * kSeqTile * 16;  // (sequence, column) slots of a stripe
   static_assert(kMT % NOUT == 0, "epilogue slots");
-  // cached: the ring holds part of one stripe's run (NT % NBUF == 0) or the
-  // runs of two stripes (NBUF == 2 NT); either way ring slots are static
-  static_assert(!CACHED || NT % NBUF == 0 || NBUF == 2 * NT, "static ring slots");
-  constexpr int SPR = CACHED && NBUF > NT ? 2 : 1;  // stripes per pass of the ring
-  constexpr int RB = NBUF / SPR;                     // ring slots per stripe
+  static_assert(!CACHED || NT % NBUF == 0, "static ring slots");
   extern __shared__ float red[];                // [a.sch][kMW][NOUT]: per wave, level-summed
   __shared__ float ssq[kMW][NBT * kSeqTile];    // per-wave sums of squares (QKV, gate/up)
   __shared__ v4u gam[MODE == MMode::kQkv ? kMaxHidden / 8 : 1];  // QKV: gamma1
@@ -335,17 +326,16 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   };
   // split inputs: this block's partial sums [stripe][slot]
   float* kp_own = ks > 1 ? a.kpart + ((size_t)blockIdx.y * G + blk) * a.kstride : nullptr;
-  // stripe si, whose items use ring slots SB .. SB + RB - 1 (SB: a constant)
-  auto stripe = [&](int si, auto sb) {
-    constexpr int SB = decltype(sb)::value;
+  // stripe si (its partial sums into LDS; the epilogue after the last stripe
+  // of a chunk)
+  auto stripe = [&](int si) {
     f4 acc[NBT];
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) acc[bt] = f4{0.f, 0.f, 0.f, 0.f};
-    for (int tt0 = 0; tt0 < ntp; tt0 += RB) {
+    for (int tt0 = 0; tt0 < ntp; tt0 += NBUF) {
 #pragma unroll
-      for (int rr = 0; rr < RB; ++rr) {
-        const int r = SB + rr;
-        const int tt = tt0 + rr;
+      for (int r = 0; r < NBUF; ++r) {
+        const int tt = tt0 + r;
         bf16x8 A[NBT];
         if constexpr (CACHED) {
           if constexpr (XPAIR) {
@@ -449,12 +439,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     __syncthreads();
     c0 = si + 1;
   };
-  for (int si = 0; si < nstr; si += SPR) {
-    stripe(si, SlotBase<0>{});
-    if constexpr (SPR == 2) {
-      if (si + 1 < nstr) stripe(si + 1, SlotBase<RB>{});
-    }
-  }
+  for (int si = 0; si < nstr; ++si) stripe(si);
 
   // ---- split inputs: the group's last block sums the parts in order -------
   if constexpr (MODE != MMode::kQkv) {
