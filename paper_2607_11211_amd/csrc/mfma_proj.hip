@@ -189,6 +189,9 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   // k-group) need the same x chunks, so lane level l loads batch tile l's and
   // the pair swaps them (one load per k-tile instead of two)
   constexpr bool XPAIR = MODE == MMode::kQkv && CACHED && NBT == 2 && NT <= 6;  // (runs of 8 tiles: spills)
+  // with one batch tile, the level lanes load two consecutive k-tiles of the
+  // same sequence slot instead and swap them (one load per two k-tiles)
+  constexpr bool XPAIR1 = MODE == MMode::kQkv && CACHED && NBT == 1 && NT % 2 == 0;
   auto ready_chunk = [&](int t, int bt) {
     return reinterpret_cast<const v4u*>(a.a_in)[((size_t)min(t, a.kt - 1) * a.nbtc + btg0 + bt) * kWave + op_lane(bt)];
   };
@@ -212,6 +215,8 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     for (int tt = 0; tt < NT; ++tt) {
       if constexpr (XPAIR) {
         acache[tt][0] = x_chunk(tbase + tt, lvl);
+      } else if constexpr (XPAIR1) {
+        if (tt % 2 == 0) acache[tt][0] = x_chunk(tbase + tt + lvl, 0);
       } else {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt)
@@ -342,6 +347,12 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
             if (si == 0) {
               const v4u own = acache[tt][0], other = dpp_swap_pair(own);
               acache[tt][1] = lvl ? own : other;
+              acache[tt][0] = lvl ? other : own;
+            }
+          } else if constexpr (XPAIR1) {
+            if (si == 0 && tt % 2 == 0) {
+              const v4u own = acache[tt][0], other = dpp_swap_pair(own);
+              acache[tt + 1][0] = lvl ? own : other;
               acache[tt][0] = lvl ? other : own;
             }
           }
