@@ -192,6 +192,16 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   // with one batch tile, the level lanes load two consecutive k-tiles of the
   // same sequence slot instead and swap them (one load per two k-tiles)
   constexpr bool XPAIR1 = MODE == MMode::kQkv && CACHED && NBT == 1 && NT % 2 == 0;
+  // ready operands of at most four sequences (one batch tile): the lanes of
+  // slots 4..7 load the next k-tile's slots 0..3 instead, so one load brings
+  // two k-tiles (row rotation by 8 hands them to the lanes of slots 0..3)
+  const bool apack = MODE != MMode::kQkv && CACHED && NBT == 1 && NT % 2 == 0 && nb <= kSeqTile / 2;
+  auto packed_chunk = [&](int t) {
+    const bool hi = bp >= kSeqTile / 2;
+    const int slot = min(hi ? bp - kSeqTile / 2 : bp, nb - 1);
+    const int tt = min(hi ? t + 1 : t, a.kt - 1);
+    return reinterpret_cast<const v4u*>(a.a_in)[((size_t)tt * a.nbtc + btg0) * kWave + 2 * slot + lvl + 16 * kg];
+  };
   auto ready_chunk = [&](int t, int bt) {
     return reinterpret_cast<const v4u*>(a.a_in)[((size_t)min(t, a.kt - 1) * a.nbtc + btg0 + bt) * kWave + op_lane(bt)];
   };
@@ -217,6 +227,8 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
         acache[tt][0] = x_chunk(tbase + tt, lvl);
       } else if constexpr (XPAIR1) {
         if (tt % 2 == 0) acache[tt][0] = x_chunk(tbase + tt + lvl, 0);
+      } else if (apack) {
+        if (tt % 2 == 0) acache[tt][0] = packed_chunk(tbase + tt);
       } else {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt)
@@ -260,6 +272,21 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   // the weight stream (built here, all at once, it held the stream ~4 us)
   if constexpr (CACHED && MODE != MMode::kQkv) {
     const v4u z = {0u, 0u, 0u, 0u};
+    if (apack) {
+      if constexpr (NBT == 1 && NT % 2 == 0) {
+#pragma unroll
+        for (int tt = 0; tt < NT; tt += 2) {
+          const v4u raw = acache[tt][0];
+          const v4u nxt = v4u{__float_as_uint(dpp_mov<kDppRowRor8>(__uint_as_float(raw.x))),
+                              __float_as_uint(dpp_mov<kDppRowRor8>(__uint_as_float(raw.y))),
+                              __float_as_uint(dpp_mov<kDppRowRor8>(__uint_as_float(raw.z))),
+                              __float_as_uint(dpp_mov<kDppRowRor8>(__uint_as_float(raw.w)))};
+          const bool lo = bp < kSeqTile / 2;
+          acache[tt][0] = lo ? raw : z;
+          acache[tt + 1][0] = lo ? nxt : z;
+        }
+      }
+    }
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
