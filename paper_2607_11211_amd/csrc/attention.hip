@@ -122,16 +122,16 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const flo
   __shared__ float osum[NG][D];
   const int tid = threadIdx.x;
   const int h = blockIdx.x, b = blockIdx.y;
-  const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + 2);
+  const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + kPartLead);
   const int grp = tid / D, e = tid % D;
   float ov[kCombineRegs];
 #pragma unroll
   for (int k = 0; k < kCombineRegs; ++k) {
     const int q = grp + NG * k;
-    ov[k] = (grp < NG && q < nsplit) ? ph[(size_t)q * (D + 2) + 2 + e] : 0.f;
+    ov[k] = (grp < NG && q < nsplit) ? ph[(size_t)q * (D + kPartLead) + kPartLead + e] : 0.f;
   }
-  const float ms = tid < nsplit ? ph[(size_t)tid * (D + 2)] : -INFINITY;
-  const float ls = tid < nsplit ? ph[(size_t)tid * (D + 2) + 1] : 0.f;
+  const float ms = tid < nsplit ? ph[(size_t)tid * (D + kPartLead)] : -INFINITY;
+  const float ls = tid < nsplit ? ph[(size_t)tid * (D + kPartLead) + 1] : 0.f;
   float M = wave_max(ms);
   if ((tid & (kWave - 1)) == 0) red[tid / kWave] = M;
   __syncthreads();
@@ -188,16 +188,16 @@ __global__ __launch_bounds__(kWave) void attn_combine_wave_kernel(const float* _
   constexpr int EPL = (D + kWave - 1) / kWave;  // o elements per lane
   const int lane = threadIdx.x;
   const int h = blockIdx.x, b = blockIdx.y;
-  const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + 2);
+  const float* ph = part + ((size_t)b * n_heads + h) * nsplit_cap * (D + kPartLead);
   const int sl = min(lane, nsplit - 1);
-  const float ms = lane < nsplit ? ph[(size_t)sl * (D + 2)] : -INFINITY;
-  const float ls = lane < nsplit ? ph[(size_t)sl * (D + 2) + 1] : 0.f;
+  const float ms = lane < nsplit ? ph[(size_t)sl * (D + kPartLead)] : -INFINITY;
+  const float ls = lane < nsplit ? ph[(size_t)sl * (D + kPartLead) + 1] : 0.f;
   float ov[NS][EPL];
 #pragma unroll
   for (int j = 0; j < NS; ++j)
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
-      ov[j][i] = ph[(size_t)min(j, nsplit - 1) * (D + 2) + 2 + min(lane + kWave * i, D - 1)];
+      ov[j][i] = ph[(size_t)min(j, nsplit - 1) * (D + kPartLead) + kPartLead + min(lane + kWave * i, D - 1)];
   const float M = wave_max(ms);
   const float f = merge_factor(ms, M);  // zero for lanes past the splits
   const float L = wave_sum(ls * f);

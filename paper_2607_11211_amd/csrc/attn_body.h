@@ -65,9 +65,7 @@ struct alignas(16) AttnSmem {
   float rl[G][kRows];
 };
 
-__device__ __forceinline__ float merge_factor(float m, float M) {
-  return (m == -INFINITY) ? 0.f : __expf(m - M);
-}
+using fasttps::merge_factor;
 
 // four codes of one 32-bit word, element 4i + k in byte k
 template <int KVF>
@@ -448,7 +446,7 @@ struct AttnBody {
 
     if (!live) return;
     const int H = a.n_heads;
-    float* part_b = a.part + (size_t)b * H * a.nsplit_cap * (D + 2);
+    float* part_b = a.part + (size_t)b * H * a.nsplit_cap * (D + kPartLead);
     for (int i = tid; i < G * D; i += kThreads) {
       const int h = i / D, e = i % D;
       float M = sm.rm[h][0];
@@ -461,8 +459,8 @@ struct AttnBody {
         L = fmaf(sm.rl[h][r], f, L);
         O = fmaf(sm.red[h][r][e], f, O);
       }
-      float* pr = part_b + ((size_t)(g * G + h) * a.nsplit_cap + s) * (D + 2);
-      io.part(pr + 2 + e, KVF == kKvBf16 ? O : O * vscale);  // an 8-bit cache's V scale
+      float* pr = part_b + ((size_t)(g * G + h) * a.nsplit_cap + s) * (D + kPartLead);
+      io.part(pr + kPartLead + e, KVF == kKvBf16 ? O : O * vscale);  // an 8-bit cache's V scale
       if (e == 0) {
         io.part(pr, M);
         io.part(pr + 1, L);

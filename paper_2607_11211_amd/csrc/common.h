@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 namespace fasttps {
@@ -40,6 +41,12 @@ __device__ __forceinline__ unsigned ld_cu(const unsigned* p) {
 __device__ __forceinline__ void st_cu(unsigned* p, unsigned v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// The log-sum-exp merge's factor of a partial softmax state with running
+// maximum m against the merged maximum M (zero for an empty state).
+__device__ __forceinline__ float merge_factor(float m, float M) {
+  return (m == -INFINITY) ? 0.f : __expf(m - M);
+}
+
 // wait for this wave's outstanding memory operations, stores included
 // (s_waitcnt vmcnt(0); expcnt and lgkmcnt left free)
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }

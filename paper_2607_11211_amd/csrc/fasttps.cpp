@@ -33,6 +33,12 @@ constexpr uint64_t kDeadMagic = 0xDEADDEADDEADDEADull;
 // for the GQA layer 512 blocks against 256 (one per CU): 193-195 -> 188-189
 // us per step (384 and 1024 slower).
 constexpr int kTargetAttnBlocks = 512;
+// One sequence: about one block per CU, so that the split partials the O
+// projection's blocks merge stay small (8 splits of the Phi-3 layer's 32
+// heads, 128 KB). Measured on MI355X (Phi-3 layer at KV 4096, HIP graph):
+// the attention is as fast at 256 blocks as at 512 (11.2-11.5 us); with 128
+// blocks it takes 12.8 us.
+constexpr int kTargetAttnBlocksOne = 256;
 constexpr int kRaggedAttnFactor = 4;
 constexpr int kAttnTile = 64;
 constexpr int kMaxSplits = 256;
@@ -353,7 +359,7 @@ int fasttps_layer_create(const fasttps_config* cfg, fasttps_layer** out) {
       cs.size() * sizeof(double),
       sn.size() * sizeof(double),
       (size_t)B * qkv_rows * sizeof(float),
-      (size_t)B * c.n_heads * nsplit_cap * (d + 2) * sizeof(float),
+      (size_t)B * c.n_heads * nsplit_cap * (d + kPartLead) * sizeof(float),
       (size_t)B * c.n_heads * d * sizeof(float),
       (size_t)B * c.hidden * sizeof(float),
       (size_t)B * c.intermediate * sizeof(float),
@@ -707,7 +713,8 @@ int attention_splits(const fasttps_layer* l, const int32_t* pos, int32_t batch, 
     total += pos[b];
     minp = std::min(minp, (int)pos[b]);
   }
-  const long target = (minp == maxp ? 1 : kRaggedAttnFactor) * (long)kTargetAttnBlocks;
+  const long target =
+      batch == 1 ? kTargetAttnBlocksOne : (minp == maxp ? 1 : kRaggedAttnFactor) * (long)kTargetAttnBlocks;
   int split_len = round_up((int)std::min<long>((total * c.n_kv_heads + target - 1) / target, maxn), kAttnTile);
   split_len = std::max(split_len, round_up(ceil_div(maxn, l->nsplit_cap), kAttnTile));
   return ceil_div(maxn, split_len);
@@ -731,7 +738,7 @@ struct StepScratch {
 size_t noalloc_layout(const fasttps_config& c, int batch, int nsplit, float* base, StepScratch* out) {
   const size_t B = batch, d = c.head_dim;
   const size_t sizes[5] = {B * (c.n_heads + 2 * c.n_kv_heads) * d * sizeof(float),
-                           B * c.n_heads * nsplit * (d + 2) * sizeof(float), B * c.n_heads * d * sizeof(float),
+                           B * c.n_heads * nsplit * (d + kPartLead) * sizeof(float), B * c.n_heads * d * sizeof(float),
                            B * c.hidden * sizeof(float), B * c.intermediate * sizeof(float)};
   size_t offs[5], total = 0;
   for (int i = 0; i < 5; ++i) {
@@ -943,8 +950,15 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   e = kvf == kKvBf16 ? launch_attention(aa, s, ev[1]) : launch_attention_kv8(aa, *sc, s, ev[1]);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   used(1);
-  if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
-  used(2);
+  // one sequence on the vector path: the O projection merges the splits in
+  // its prologue, one launch fewer (Phi-3 layer on MI355X, HIP graph: 60.1 ->
+  // 57.8 us per step at KV 4096, 54.5 -> 52.0 us at KV 1024); otherwise the
+  // combine kernel
+  const bool merge_in_o = !mfma && batch == 1 && oproj_merge_supported(c.n_heads, (int)d, nsplit, (int)D);
+  if (!merge_in_o) {
+    if ((e = launch_attention_combine(aa, s, ev[2])) != hipSuccess) return hip_fail(e, "attention combine launch");
+    used(2);
+  }
 
   if (mfma) {
     MfmaArgs m = mfma_args(lt.o, w->t_o, (int)D, c.n_heads * (int)d);
@@ -968,7 +982,18 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
     m.out_bf16 = static_cast<uint16_t*>(y);
     if ((e = launch_mfma_down(m, s, ev[5])) != hipSuccess) return hip_fail(e, "mlp down launch");
   } else {
-    if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
+    if (merge_in_o) {
+      MergeArgs ma{};
+      ma.part = S.part;
+      ma.o = S.o;
+      ma.nsplit = nsplit;
+      ma.nsplit_cap = S.nsplit_cap;
+      ma.n_heads = c.n_heads;
+      ma.head_dim = (int)d;
+      if ((e = launch_oproj_merge(oa, ma, s, ev[3])) != hipSuccess) return hip_fail(e, "o-proj launch");
+    } else if ((e = launch_oproj_residual(oa, s, ev[3])) != hipSuccess) {
+      return hip_fail(e, "o-proj launch");
+    }
     if (mlp_fused) {
       MlpFusedArgs mf{};
       mf.w_down_slices = w->w_down_slices;

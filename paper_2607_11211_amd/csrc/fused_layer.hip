@@ -170,12 +170,12 @@ __global__ __launch_bounds__(kFThreads) void fused_layer_kernel(FusedArgs f) {
     const bool act = t < per * nsplit;
     const int el = min(e0 + (act ? t / nsplit : 0), nel - 1), sp = act ? t % nsplit : 0;
     const int h = el / D_, e = el % D_;
-    const float* pr = f.attn.part + ((size_t)h * f.attn.nsplit_cap + sp) * (D + 2);
+    const float* pr = f.attn.part + ((size_t)h * f.attn.nsplit_cap + sp) * (D + kPartLead);
     float* mm = stage;                                 // [per][64] m, then l, then o of each split
     float* ll = stage + (size_t)per * kWave;
     float* oo = stage + 2 * (size_t)per * kWave;
     wait_phase(f, 1, epoch, wave);
-    const float mv = ld_c(pr), lv = ld_c(pr + 1), ov = ld_c(pr + 2 + e);
+    const float mv = ld_c(pr), lv = ld_c(pr + 1), ov = ld_c(pr + kPartLead + e);
     if (act) {
       const int r = t / nsplit;
       mm[r * kWave + sp] = mv;

@@ -120,7 +120,146 @@ hipError_t launch_mode(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
   return launch_bt<1, MODE>(a, s, ev);
 }
 
+// ---- the O projection with the split merge in its prologue (batch 1) ------
+
+// the activation from an LDS stage
+struct StageIO {
+  const float* stage;
+  __device__ __forceinline__ float4 act4(const GemvArgs& a, int b, int i4) const {
+    return reinterpret_cast<const float4*>(stage + (size_t)b * a.din)[i4];
+  }
+  __device__ __forceinline__ float res(const GemvArgs& a, size_t o) const { return a.res_f32[o]; }
+  __device__ __forceinline__ void out(const GemvArgs& a, size_t o, float v) const { a.out[o] = v; }
+};
+
+constexpr int kMergeThreads = kWaves * kWave;
+// rows in flight per wave: one, as in the separate O projection (two or
+// three, the block's whole share of W_o primed before the merge, were slower
+// on MI355X: the Phi-3 layer step 59.0 -> 59.6 and 60.4 us)
+constexpr int kMergeRing = 1;
+static_assert(kMergeMaxElems <= 4 * kMergeThreads, "four o elements per thread");
+
+// Every block: (1) loads, for its thread's four elements of o, the partial o
+// values and the (m, l) of every split of their head, then issues its first
+// weight rows; (2) merges the splits (M = max m, factors e^(m - M),
+// L = sum l e^(m - M), o = sum o e^(m - M) / L, as the combine kernel does)
+// into the LDS stage, with no block barrier until the stage is complete; (3)
+// streams its W_o rows against the stage with the residual added.
+template <int MAXCH, int NSEG_H, int NS>
+__global__ __launch_bounds__(kMergeThreads) void oproj_merge_kernel(GemvArgs a, MergeArgs m) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  constexpr int NBUF = kMergeRing;
+  const int tid = threadIdx.x;
+  const int D = m.head_dim, ns = m.nsplit, nel = m.n_heads * D;
+  const int rs = D + kPartLead;  // floats per split record
+  float* stage = lds;            // o [H d]
+  float* gl = lds + nel;
+
+  // (1) the partials (clamped, unconditional loads; o is 16-byte aligned in
+  // every record and D is a multiple of 4, so the four elements share a head)
+  const int e = 4 * min(tid, nel / 4 - 1);
+  const float* ph = m.part + (size_t)(e / D) * m.nsplit_cap * rs;
+  float4 ov[NS];
+  float2 ml[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const float* r = ph + (size_t)min(s, ns - 1) * rs;
+    ml[s] = *reinterpret_cast<const float2*>(r);
+    ov[s] = *reinterpret_cast<const float4*>(r + kPartLead + e % D);
+  }
+  gemv::GemvBody<1, MAXCH, NSEG_H, NBUF, Mode::kResidual, StageIO> body(a, StageIO{stage}, gl, blockIdx.x, gridDim.x,
+                                                                        0, tid);
+  body.load_resid();
+  __builtin_amdgcn_sched_barrier(0);  // the weight loads go out after the partials' and the residual's
+  body.prime();
+
+  // (2) the merge of this thread's head
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < ns) M = fmaxf(M, ml[s].x);
+  float L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const float f = s < ns ? merge_factor(ml[s].x, M) : 0.f;
+    L = fmaf(ml[s].y, f, L);
+    acc.x = fmaf(ov[s].x, f, acc.x);
+    acc.y = fmaf(ov[s].y, f, acc.y);
+    acc.z = fmaf(ov[s].z, f, acc.z);
+    acc.w = fmaf(ov[s].w, f, acc.w);
+  }
+  if (tid < nel / 4) {
+    const float4 v = make_float4(acc.x / L, acc.y / L, acc.z / L, acc.w / L);
+    *reinterpret_cast<float4*>(stage + e) = v;
+    if (blockIdx.x == 0) *reinterpret_cast<float4*>(m.o + e) = v;
+  }
+  __syncthreads();
+
+  // (3) the projection
+  body.load_act();
+  body.run();
+}
+
+template <int MAXCH, int NSEG_H>
+hipError_t launch_merge_shape(const GemvArgs& a, const MergeArgs& m, hipStream_t s, KernelEvents ev) {
+  using Body = gemv::GemvBody<1, MAXCH, NSEG_H, kMergeRing, Mode::kResidual, StageIO>;
+  const int nblk = a.rows < kNumCu ? a.rows : kNumCu;
+  constexpr int NG = kWaves / NSEG_H;
+  if (NSEG_H == 1 && (((a.rows + nblk - 1) / nblk) + NG - 1) / NG > kWave) return hipErrorInvalidValue;
+  const size_t lds = ((size_t)m.n_heads * m.head_dim + Body::lds_floats(a.rows, nblk)) * sizeof(float);
+  if (m.nsplit <= 4)
+    return ext_launch(oproj_merge_kernel<MAXCH, NSEG_H, 4>, dim3(nblk), dim3(kMergeThreads), lds, s, ev, a, m);
+  if (m.nsplit <= 8)
+    return ext_launch(oproj_merge_kernel<MAXCH, NSEG_H, 8>, dim3(nblk), dim3(kMergeThreads), lds, s, ev, a, m);
+  return ext_launch(oproj_merge_kernel<MAXCH, NSEG_H, 16>, dim3(nblk), dim3(kMergeThreads), lds, s, ev, a, m);
+}
+
+template <int MAXCH>
+hipError_t launch_merge_seg(const GemvArgs& a, const MergeArgs& m, int nseg_h, hipStream_t s, KernelEvents ev) {
+  switch (nseg_h) {
+    case 1: return launch_merge_shape<MAXCH, 1>(a, m, s, ev);
+    case 2: return launch_merge_shape<MAXCH, 2>(a, m, s, ev);
+    case 4: return launch_merge_shape<MAXCH, 4>(a, m, s, ev);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// the shape launch_bt<1, kResidual> picks for din inputs (chunks per lane,
+// segments per half row), restricted to what the merge kernel instantiates
+bool merge_shape(int din, int* maxch, int* nseg_h) {
+  const int nch = din / 8;
+  const int ns = segments_for(din, max_chunks(1, false));
+  if (ns > kWaves) return false;
+  const int per = (nch + ns * kWave - 1) / (ns * kWave);
+  if (per > 3 || ns > 4) return false;
+  *maxch = per < 1 ? 1 : per;
+  *nseg_h = ns;
+  return true;
+}
+
 }  // namespace
+
+bool oproj_merge_supported(int n_heads, int head_dim, int nsplit, int rows) {
+  int mc, sg;
+  const int nel = n_heads * head_dim;
+  return nsplit >= 1 && nsplit <= kMergeMaxSplits && nel <= kMergeMaxElems && head_dim % 4 == 0 &&
+         merge_shape(nel, &mc, &sg) && rows >= 1;
+}
+
+hipError_t launch_oproj_merge(const GemvArgs& a, const MergeArgs& m, hipStream_t s, KernelEvents ev) {
+  if (a.batch != 1 || !oproj_merge_supported(m.n_heads, m.head_dim, m.nsplit, a.rows) ||
+      a.din != m.n_heads * m.head_dim)
+    return hipErrorInvalidValue;
+  int maxch, nseg_h;
+  merge_shape(a.din, &maxch, &nseg_h);
+  switch (maxch) {
+    case 1: return launch_merge_seg<1>(a, m, nseg_h, s, ev);
+    case 2: return launch_merge_seg<2>(a, m, nseg_h, s, ev);
+    case 3: return launch_merge_seg<3>(a, m, nseg_h, s, ev);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 FusedShape::Gemv gemv_shape_b1(int din, bool gate_up) {
   const int nh = gate_up ? 2 : 1;

@@ -142,7 +142,12 @@ struct GemvBody {
 
   // ---- 1. residuals of this wave's rows, its activation chunks, the gains --
   __device__ __forceinline__ void load_inputs() {
-    // residual of (b, k-th row of this wave) in lane b * nmine + k
+    load_resid();
+    load_act();
+  }
+
+  // residual of (b, k-th row of this wave) in lane b * nmine + k
+  __device__ __forceinline__ void load_resid() {
     if (has_residual<MODE>()) {
       const int nm = nmine > 0 ? nmine : 1;
       const int q = min(lane, nb * nm - 1);
@@ -150,6 +155,10 @@ struct GemvBody {
       const size_t o = (size_t)(b0 + qb) * a.rows + blk + (size_t)G * min(grp + NG * qk, nrow - 1);
       resid = MODE == Mode::kResidual ? bf16_to_f32(a.x_bf16[o]) : io.res(a, o);
     }
+  }
+
+  // the activation values of this wave's chunks, and the gains
+  __device__ __forceinline__ void load_act() {
 #pragma unroll
     for (int j = 0; j < MAXCH; ++j) {
       const int c = min(cbase + lane + kWave * j, nch - 1);

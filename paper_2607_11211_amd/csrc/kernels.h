@@ -58,6 +58,22 @@ hipError_t launch_gate_up(const GemvArgs& a, hipStream_t s, KernelEvents ev = {}
 // out = W act (fp32 in and out), rows of `ld` elements (the op-by-op baseline).
 hipError_t launch_gemv_plain(const GemvArgs& a, hipStream_t s, KernelEvents ev = {});
 
+// The O projection of one sequence with the merge of the attention's split
+// partials in its prologue (gemv.hip), in place of a separate combine kernel:
+// every block merges all heads' splits into o in LDS (the log-sum-exp merge
+// of Alg. 3's softmax over the splits), then streams its rows of W_o as
+// launch_oproj_residual does; block 0 also stores o.
+struct MergeArgs {
+  const float* part;  // [H, nsplit_cap, d + kPartLead] (m, l, -, -, o) of each split, sequence 0
+  float* o;           // [H d] fp32
+  int nsplit, nsplit_cap, n_heads, head_dim;
+};
+constexpr int kMergeMaxSplits = 16;
+constexpr int kMergeMaxElems = 4096;  // H d
+bool oproj_merge_supported(int n_heads, int head_dim, int nsplit, int rows);
+// a: the O projection's GemvArgs (batch 1; in_f32 unused)
+hipError_t launch_oproj_merge(const GemvArgs& a, const MergeArgs& m, hipStream_t s, KernelEvents ev = {});
+
 // The fused MLP (mlp_fused.hip): gate/up + siLu_Mul of a slice of units per
 // block with h^sm kept in LDS, the slice's down-projection partial of y, and
 // a fixed-order sum of the partials with the residual.
@@ -117,13 +133,17 @@ hipError_t launch_mfma_down(const MfmaArgs& a, hipStream_t s, KernelEvents ev = 
 hipError_t launch_tile_weights(const uint16_t* src, const uint16_t* up, int rows, int din, int ld, int ns, int kt,
                                int rh, uint16_t* dst, hipStream_t s);
 
+// A split's partial softmax state in the attention's scratch: m, l, two unused
+// floats, then o[d], so that o starts on a 16-byte boundary.
+constexpr int kPartLead = 4;
+
 struct AttnArgs {
   const float* qkv;        // [batch, (H + 2 H_kv) d] fp32, before RoPE
   const double* rope_cos;  // [N_max, d/2]
   const double* rope_sin;  // [N_max, d/2]
   void* k_cache;           // [B, H_kv, N_max, d], bf16 or 8-bit codes
   void* v_cache;
-  float* part;             // [batch, H, nsplit_cap, d + 2] split partials (m, l, o)
+  float* part;             // [batch, H, nsplit_cap, d + kPartLead] split partials (m, l, -, -, o)
   float* o;                // [batch, H d] fp32
   uint16_t* o_operand;     // if set: o split for the MFMA O projection [kt][o_nbtc][64][8]
   int o_nbtc;
