@@ -60,6 +60,12 @@ SMALL = [
     # block combine's threads in use)
     LayerConfig(name="s_ctx128k", index=20, batch=1, hidden=256, n_heads=1, n_kv_heads=1, head_dim=64,
                 intermediate=688, rope_base=500000.0, max_seq=131136, pos=(131072,)),
+    # one sequence: the O projection merges up to 16 splits itself (16 here), past that the
+    # combine kernel runs (17)
+    LayerConfig(name="s_merge16", index=25, batch=1, hidden=768, n_heads=8, n_kv_heads=8, head_dim=96,
+                intermediate=1024, rope_base=10000.0, max_seq=1100, pos=(1024,)),
+    LayerConfig(name="s_merge17", index=26, batch=1, hidden=768, n_heads=8, n_kv_heads=8, head_dim=96,
+                intermediate=1024, rope_base=10000.0, max_seq=1100, pos=(1040,)),
     # group 2, batch 9 (two batch tiles of the projections)
     LayerConfig(name="s_g2_b9", index=13, batch=9, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200, pos=(0, 3, 17, 64, 100, 128, 150, 190, 199)),
