@@ -206,8 +206,9 @@ FASTTPS_API int fasttps_decode_step_unfused(fasttps_layer* layer, const fasttps_
  *                        MFMA tile order (about twice the weight memory, or
  *                        the tiles only: fasttps_set_weight_layout)
  *   FASTTPS_GEMM_FUSED   one sequence in one persistent kernel (below); a
- *                        measured alternative, slower on MI355X than the six
- *                        kernels of the vector path replayed from a HIP graph
+ *                        measured alternative, slower on MI355X than the
+ *                        separate kernels of the vector path replayed from a
+ *                        HIP graph
  *   FASTTPS_GEMM_AUTO    (default) the matrix path from 2 sequences up where
  *                        the weights carry the tiles, else the vector path
  * At batch 8-16 the projections are dense enough that the multiply-adds
@@ -348,7 +349,9 @@ FASTTPS_API int fasttps_validate_step(const fasttps_config* cfg, const void* x, 
  * Kernel k is named by fasttps_kernel_name(k). Steps beyond max_steps run
  * untimed. Not for use under stream capture. */
 #define FASTTPS_NUM_KERNELS 7  /* the six kernels of the separate path, then the fused kernel;
-                                  a kernel a step does not launch reads 0 */
+                                  a kernel a step does not launch reads 0 (the combine at
+                                  batch 1, where the O projection merges the splits and is
+                                  timed as kernel 3) */
 FASTTPS_API int fasttps_profile_begin(fasttps_layer* layer, int32_t max_steps);
 FASTTPS_API int fasttps_profile_end(fasttps_layer* layer, float* ms, int32_t max_steps, int32_t* n_steps);
 FASTTPS_API const char* fasttps_kernel_name(int32_t k);

@@ -172,10 +172,14 @@ __device__ __forceinline__ void tile_load_contig(v4u (&k)[NC], v4u (&v)[NC], con
   }
 }
 
-// Plain global-memory IO of the attention kernel.
+// Plain global-memory IO of the attention kernel. rec() is where the split's
+// record (m, l, -, -, o) of query head `head` of sequence b goes.
 struct GlobalIO {
   __device__ __forceinline__ float qkv(const AttnArgs& a, size_t i) const { return a.qkv[i]; }
   __device__ __forceinline__ void part(float* p, float v) const { *p = v; }
+  __device__ __forceinline__ float* rec(const AttnArgs& a, int b, int head, int s, int D) const {
+    return a.part + (((size_t)b * a.n_heads + head) * a.nsplit_cap + s) * (D + kPartLead);
+  }
 };
 
 // PBF16: the softmax weights enter PV rounded to bf16, as FlashAttention's
@@ -216,16 +220,18 @@ struct AttnBody {
   float q0, q1, k0, k1, v0;
   Chunk kr[NRING][NC], vr[NRING][NC];
 
+  // nsplit_: the splits the tiles are dealt to (0: a.nsplit)
   __device__ __forceinline__ AttnBody(const AttnArgs& a_, IO io_, Smem& sm_, int tid_, int s_, int g_, int b_,
-                                      bool live_, v4u* xk_ = nullptr, v4u* xv_ = nullptr)
+                                      bool live_, v4u* xk_ = nullptr, v4u* xv_ = nullptr, int nsplit_ = 0)
       : a(a_), io(io_), sm(sm_), tid(tid_), s(s_), g(g_), b(b_), live(live_) {
+    const int nsp = nsplit_ ? nsplit_ : a.nsplit;
     xk = xk_ + (tid_ / kWave) * SPAN;
     xv = xv_ + (tid_ / kWave) * SPAN;
     P = a.pos.p[b];
     // tiles s, s + nsplit, ... of the sequence's cached entries [0, P); the
     // new entry P is added from LDS by the split whose tile index holds it
     start = s * kTile;
-    stride = a.nsplit * kTile;
+    stride = nsp * kTile;
     end = live ? P : start;
     last = max(P - 1, 0);  // loads past the end read this cached row (masked); slot P is never read
                            // unless P = 0, where the clamped prime loads read slot 0 and discard it
@@ -234,7 +240,7 @@ struct AttnBody {
     Vc = reinterpret_cast<const Chunk*>(static_cast<const uint8_t*>(a.v_cache) + head_off);
     j = tid >> 2;
     seg = tid & 3;
-    own_new = live && (P / kTile) % a.nsplit == s;  // the split whose tile holds slot P
+    own_new = live && (P / kTile) % nsp == s;  // the split whose tile holds slot P
     pj = tid % HALF;
     ph = min(tid / HALF, G - 1);
   }
@@ -445,8 +451,6 @@ struct AttnBody {
     __syncthreads();
 
     if (!live) return;
-    const int H = a.n_heads;
-    float* part_b = a.part + (size_t)b * H * a.nsplit_cap * (D + kPartLead);
     for (int i = tid; i < G * D; i += kThreads) {
       const int h = i / D, e = i % D;
       float M = sm.rm[h][0];
@@ -459,7 +463,7 @@ struct AttnBody {
         L = fmaf(sm.rl[h][r], f, L);
         O = fmaf(sm.red[h][r][e], f, O);
       }
-      float* pr = part_b + ((size_t)(g * G + h) * a.nsplit_cap + s) * (D + kPartLead);
+      float* pr = io.rec(a, b, g * G + h, s, D);
       io.part(pr + kPartLead + e, KVF == kKvBf16 ? O : O * vscale);  // an 8-bit cache's V scale
       if (e == 0) {
         io.part(pr, M);

@@ -789,8 +789,8 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   // one sequence: the whole step as one persistent kernel, on request
   // (FASTTPS_GEMM_FUSED), where it is built for the shape and the step is the
   // plain bf16-cache step. Not the automatic choice: on MI355X its phase
-  // hand-overs through coherent flags cost more than the six kernels'
-  // boundaries in a HIP graph (85 vs 62 us per Phi-3 layer at KV 4096).
+  // hand-overs through coherent flags cost more than the separate kernels'
+  // boundaries in a HIP graph (67.6 vs 57.7 us per Phi-3 layer at KV 4096).
   FusedShape fsh{};
   fsh.head_dim = (int)d;
   fsh.group = c.n_heads / c.n_kv_heads;
@@ -798,8 +798,9 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   fsh.o = gemv_shape_b1(c.n_heads * (int)d, false);
   fsh.gu = gemv_shape_b1((int)D, true);
   fsh.down = gemv_shape_b1(c.intermediate, false);
-  const bool fused_ok = batch == 1 && kvf == kKvBf16 && l->p_bf16 == 0 && nsplit <= 64 &&
-                        ceil_div(c.n_heads * (int)d, kFusedBlocks) * nsplit <= 1024 && fused_layer_supported(fsh);
+  const bool fused_ok = batch == 1 && kvf == kKvBf16 && l->p_bf16 == 0 && nsplit <= fused_layer_max_splits() &&
+                        nsplit * c.n_kv_heads <= fused_layer_grid() && c.n_heads * (int)d <= 4096 &&
+                        fused_layer_supported(fsh);
   const bool fused = !mfma && !S.noalloc && !mlp_fused && l->gemm_path == FASTTPS_GEMM_FUSED;
   if (fused && !fused_ok)
     return fail(FASTTPS_ERR_UNSUPPORTED, "the fused kernel is built for one sequence of the Phi-3-mini layer shape");

@@ -195,6 +195,8 @@ struct FusedShape {
   Gemv q, o, gu, down;
 };
 bool fused_layer_supported(const FusedShape& sh);
+int fused_layer_max_splits();  // attention splits per KV head the kernel merges
+int fused_layer_grid();        // its blocks (one (KV head, split) item each at most)
 hipError_t launch_fused_layer(const FusedArgs& f, const FusedShape& sh, hipStream_t s, KernelEvents ev = {});
 // the launch shape the separate GEMV kernels use for one sequence
 FusedShape::Gemv gemv_shape_b1(int din, bool gate_up);
