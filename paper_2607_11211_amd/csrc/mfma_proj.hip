@@ -63,7 +63,13 @@ constexpr int kMGrid = 256;       // blocks (one per CU)
 constexpr int kSeqTile = 8;       // sequences per MFMA (two levels each)
 constexpr int kGroupSeq = 16;     // sequences per block row of the grid (two batch tiles)
 constexpr int kMaxStripesIn = 1024;  // stripes of the O projection's sums of squares (D <= 8192 at 8 rows)
-constexpr int kMaxChunkBytes = 40 * 1024;  // LDS for the partial sums of one chunk of stripes
+// LDS for the partial sums of one chunk of stripes: every chunk ends in a
+// block barrier, so a chunk holds all of a block's stripes where it can (four
+// at 16 sequences). With 40 KB the 16-sequence Phi-3 layer's QKV (3 stripes
+// per block) and gate/up (4) projections met at a barrier mid-stream: on
+// MI355X 64 KB gave QKV 15.9 -> 14.3 us, gate/up 21.4 -> 20.3 us and the
+// layer step 148 -> 144 us
+constexpr int kMaxChunkBytes = 64 * 1024;
 constexpr int kMaxHidden = 8192;           // inputs of the QKV projection (gamma1 in LDS)
 constexpr int kMaxParts = 4;               // input parts of a split projection
 
