@@ -76,10 +76,14 @@ KERNEL_SOURCES = {
     "attention": [CSRC + "attention.hip", CSRC + "attn_body.h", CSRC + "common.h", CSRC + "kernels.h",
                   CSRC + "fasttps.cpp"],
     "mfma": [CSRC + "mfma_proj.hip", CSRC + "common.h", CSRC + "kernels.h"],
+    # one sequence: the O projection also reads the attention's split records
+    # (their count is chosen on the host)
+    "gemv_merge": [CSRC + "gemv.hip", CSRC + "gemv_body.h", CSRC + "common.h", CSRC + "kernels.h",
+                   CSRC + "fasttps.cpp"],
     "fused": [CSRC + "fused_layer.hip", CSRC + "gemv_body.h", CSRC + "attn_body.h", CSRC + "common.h",
               CSRC + "kernels.h", CSRC + "fasttps.cpp"],
 }
-KERNEL_GROUP = {"rmsnorm_qkv": "gemv", "oproj_residual": "gemv", "mlp_gate_up": "gemv", "mlp_down": "gemv",
+KERNEL_GROUP = {"rmsnorm_qkv": "gemv", "oproj_residual": "gemv_merge", "mlp_gate_up": "gemv", "mlp_down": "gemv",
                 "attention": "attention", "attn_combine": "attention", "fused_layer": "fused"}
 
 
