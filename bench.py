@@ -227,11 +227,16 @@ def cpu_baseline(cfg, seconds: float, kv_fmt: str = "bf16"):
             "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
 
 
-def read_ceiling(nbytes: int = 4 << 30):
+def read_ceiling(nbytes: int = 4 << 30, same_size: int = 0):
     """Measured HBM read rates in the same run: the stream-read probe (16-byte
     loads over 4 GiB, 16 times the Infinity Cache) at a few launch shapes, best
     of three launches each, with plain loads and with the non-temporal policy
-    of the weight streams. Returns {flavour: (GB/s, blocks, unroll)}."""
+    of the weight streams. Returns {flavour: (GB/s, blocks, unroll)}. With
+    same_size > 0 also "same_size": the best rate of one non-temporal read
+    launch of that many bytes (slices at eight offsets of the 4 GiB buffer, so
+    no slice is in the Infinity Cache from the one before), timed like the
+    layer's kernels: one launch between two events on its stream, launch and
+    ramp included."""
     import ctypes
     import torch
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_11211_amd", "libfasttps_probe.so"))
@@ -255,6 +260,21 @@ def read_ceiling(nbytes: int = 4 << 30):
                     gbps = nbytes / (ms.value * 1e-3) / 1e9
                     if flavour not in best or gbps > best[flavour][0]:
                         best[flavour] = (gbps, blocks, unroll)
+    if same_size > 0:
+        n = (min(same_size, nbytes // 8) + 15) // 16 * 16
+        for blocks in (1024, 2048, 8192):
+            for unroll in (1, 2, 4, 8):
+                for k in range(8):
+                    off = (k * (nbytes // 8)) // 256 * 256
+                    ms = ctypes.c_float()
+                    rc = lib.fasttps_probe_stream_read(ctypes.c_void_p(buf.data_ptr() + off), n,
+                                                       ctypes.c_void_p(sink.data_ptr()), blocks, unroll, 1,
+                                                       ctypes.c_void_p(stream), ctypes.byref(ms))
+                    if rc != 0:
+                        raise RuntimeError(f"fasttps_probe_stream_read failed: {rc}")
+                    gbps = n / (ms.value * 1e-3) / 1e9
+                    if "same_size" not in best or gbps > best["same_size"][0]:
+                        best["same_size"] = (gbps, blocks, unroll)
     del buf
     torch.cuda.empty_cache()
     return best
@@ -676,10 +696,14 @@ def main() -> int:
     ms_step, us_layer, gbps = t["ms_step"], t["us_layer"], t["gbps"]
     roofline = dominant_roofline(kb, kern_us)
 
-    ceil = read_ceiling()
+    dom_bytes = roofline["algorithmic_bytes"] if roofline else 0
+    ceil = read_ceiling(same_size=dom_bytes)
     for fl, (g_, b_, u_) in ceil.items():
-        log(f"read ceiling (stream-read probe, 4 GiB, {fl} loads): {g_:.0f} GB/s at {b_} blocks, unroll {u_}")
+        what = f"{dom_bytes / 1e6:.1f} MB, one launch" if fl == "same_size" else "4 GiB"
+        log(f"read ceiling (stream-read probe, {what}, {fl} loads): {g_:.0f} GB/s at {b_} blocks, unroll {u_}")
     ceiling, c_blocks, c_unroll = ceil["nontemporal"]
+    if roofline and roofline.get("achieved") and "same_size" in ceil:
+        roofline["frac_of_same_size_read"] = round(roofline["achieved"] / ceil["same_size"][0], 4)
     wbytes = cfg.weight_bytes()
 
     workloads = None
@@ -710,7 +734,14 @@ def main() -> int:
                          "method": f"libfasttps_probe stream read of 4 GiB with 16-byte non-temporal loads, best "
                                    f"launch ({c_blocks} blocks x 256 threads, {c_unroll} loads in flight per thread)",
                          "plain_loads_gbps": round(ceil["plain"][0], 1),
-                         "layer_frac_of_ceiling": round(gbps / ceiling, 4)},
+                         "layer_frac_of_ceiling": round(gbps / ceiling, 4),
+                         "same_size_read": ({"bytes": dom_bytes, "gbps": round(ceil["same_size"][0], 1),
+                                             "method": "one non-temporal stream-read launch of the dominant "
+                                                       "kernel's algorithmic bytes between two events, best of "
+                                                       "8 slices x 12 launch shapes (best "
+                                                       f"{ceil['same_size'][1]} blocks, unroll "
+                                                       f"{ceil['same_size'][2]})"}
+                                            if "same_size" in ceil else None)},
         "weights_only_gbps": round(wbytes / (us_layer * 1e-6) / 1e9, 1),
         "us_per_layer_p10_p50_p90": ([round(float(np.percentile(step_samples, q)) * 1e3 / nl, 3)
                                       for q in (10, 50, 90)] if step_samples is not None else None),
