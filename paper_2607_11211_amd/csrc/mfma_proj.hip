@@ -85,10 +85,9 @@ __device__ __forceinline__ uint32_t bf16_bits(float f) {
   return f != f ? ((u >> 16) | 0x40u) : r;
 }
 
-// level `lvl` of the exact split of 8 values of at most 16 significant bits
-// (products of two bf16 numbers): hi is v truncated to bf16, lo = v - hi has
-// at most 8 significant bits, so it is a bf16 number too and hi + lo = v.
-__device__ __forceinline__ v4u split8_exact(const float (&v)[8], int lvl) {
+// level `lvl` of the same split, selected per element (the form of the
+// widest cached runs, whose registers the lean form below does not fit)
+__device__ __forceinline__ v4u split8_exact_sel(const float (&v)[8], int lvl) {
   uint32_t h[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -96,6 +95,20 @@ __device__ __forceinline__ v4u split8_exact(const float (&v)[8], int lvl) {
     h[j] = lvl ? __float_as_uint(v[j] - __uint_as_float(u & 0xFFFF0000u)) >> 16 : u >> 16;
   }
   return v4u{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+}
+
+// One level of the exact split of 8 values of at most 16 significant bits
+// (products of two bf16 numbers), chosen by the mask m of the lane's level:
+// with m = 0 the value stays, and its top half is hi, its truncation to bf16;
+// with m = 0xFFFF0000 the truncation is subtracted, leaving lo = v - hi, which
+// has at most 8 significant bits, so its top half is a bf16 number too and
+// hi + lo = v. The top halves of two words pack with one byte permute.
+__device__ __forceinline__ v4u split8_exact(const float (&v)[8], uint32_t m) {
+  uint32_t t[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) t[j] = __float_as_uint(v[j] - __uint_as_float(__float_as_uint(v[j]) & m));
+  return v4u{__builtin_amdgcn_perm(t[1], t[0], 0x07060302u), __builtin_amdgcn_perm(t[3], t[2], 0x07060302u),
+             __builtin_amdgcn_perm(t[5], t[4], 0x07060302u), __builtin_amdgcn_perm(t[7], t[6], 0x07060302u)};
 }
 
 // element offset of (sequence b, input k, level) in an operand buffer of
@@ -165,22 +178,31 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     }
   }
 
-  // the QKV operand of k-tile t for batch tile bt, built from x and gamma1;
-  // zero past the matrix or the batch. ss: the lane's sum of x^2 (level-0
-  // lanes, real entries; else 0).
-  auto qkv_operand = [&](v4u xv, v4u gv, int t, int bt, float& ss) -> v4u {
+  // The QKV operand of one k-tile and batch tile: x * gamma1 of this lane's
+  // chunk (exact: two bf16 factors), split into the lane's level; s2: the
+  // chunk's sum of x^2. gamma1 comes zero past the matrix (gamma_tile), so
+  // those products are zero; the caller drops their sums of squares.
+  // Sequence slots past the batch hold the last sequence's x, and no
+  // epilogue reads their rows.
+  // The lean form runs wherever the registers allow it: on MI355X it took the
+  // 16-sequence Phi-3 QKV projection from 14.2 to 13.6 us (the build is most
+  // of that kernel's vector work); with two batch tiles and runs of 7 or 8
+  // cached k-tiles it spilled inside the stripe loop (16-sequence GQA shape:
+  // 15.6 -> 17.5 us), so those keep the per-element form (qkv_operand_sel).
+  constexpr bool LEAN = !(NBT == 2 && NT >= 7);
+  const uint32_t lvmask = lvl ? 0xFFFF0000u : 0u;
+  auto qkv_operand = [&](v4u xv, v4u gv, float& s2) -> v4u {
     float xf[8], g[8], v[8];
     unpack8(xv, xf);
     unpack8(gv, g);
-    const bool ok = t < a.kt && 32 * t + 8 * kg < a.din && bt * kSeqTile + bp < nb;
-    float s2 = 0.f;
+    float s = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      v[e] = ok ? xf[e] * g[e] : 0.f;  // exact: two bf16 factors
-      s2 = fmaf(xf[e], xf[e], s2);
+      v[e] = xf[e] * g[e];
+      s = fmaf(xf[e], xf[e], s);
     }
-    ss = ok && lvl == 0 ? s2 : 0.f;
-    return split8_exact(v, lvl);
+    s2 = s;
+    return split8_exact(v, lvmask);
   };
   auto x_chunk = [&](int t, int bt) {
     const int k0 = min(32 * min(t, a.kt - 1) + 8 * kg, a.din - 8);
@@ -190,6 +212,29 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   auto g_chunk = [&](int t) {  // from the LDS copy (this wave's entries)
     const int k0 = min(32 * min(t, a.kt - 1) + 8 * kg, a.din - 8);
     return gam[k0 / 8];
+  };
+  // the per-element form: zero past the matrix or the batch; ss: the lane's
+  // sum of x^2 (level-0 lanes, real entries; else 0)
+  auto qkv_operand_sel = [&](v4u xv, v4u gv, int t, int bt, float& ss) -> v4u {
+    float xf[8], g[8], v[8];
+    unpack8(xv, xf);
+    unpack8(gv, g);
+    const bool ok = t < a.kt && 32 * t + 8 * kg < a.din && bt * kSeqTile + bp < nb;
+    float s2 = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[e] = ok ? xf[e] * g[e] : 0.f;
+      s2 = fmaf(xf[e], xf[e], s2);
+    }
+    ss = ok && lvl == 0 ? s2 : 0.f;
+    return split8_exact_sel(v, lvl);
+  };
+  // gamma1 of k-tile t for this lane's k-group, zero past the matrix; ok:
+  // whether the chunk is inside it
+  auto gamma_tile = [&](int t, bool& ok) {
+    ok = t < a.kt && 32 * t + 8 * kg < a.din;
+    const v4u z = {0u, 0u, 0u, 0u};
+    return ok ? g_chunk(t) : z;
   };
   // QKV with two batch tiles: the two level lanes of a (sequence slot,
   // k-group) need the same x chunks, so lane level l loads batch tile l's and
@@ -389,24 +434,41 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
               acache[tt][0] = lvl ? other : own;
             }
           }
-#pragma unroll
-          for (int bt = 0; bt < NBT; ++bt) {
+          if constexpr (LEAN) {
             if (MODE == MMode::kQkv && si == 0) {
-              float s2;
-              acache[tt][bt] = qkv_operand(acache[tt][bt], g_chunk(tbase + tt), tbase + tt, bt, s2);
-              ssp[bt] += s2;
+              bool gok;
+              const v4u g = gamma_tile(tbase + tt, gok);
+#pragma unroll
+              for (int bt = 0; bt < NBT; ++bt) {
+                float s2;
+                acache[tt][bt] = qkv_operand(acache[tt][bt], g, s2);
+                ssp[bt] += gok ? s2 : 0.f;
+              }
             }
-            A[bt] = as_bf16x8(acache[tt][bt]);
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) A[bt] = as_bf16x8(acache[tt][bt]);
+          } else {
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+              if (MODE == MMode::kQkv && si == 0) {
+                float s2;
+                acache[tt][bt] = qkv_operand_sel(acache[tt][bt], g_chunk(tbase + tt), tbase + tt, bt, s2);
+                ssp[bt] += s2;
+              }
+              A[bt] = as_bf16x8(acache[tt][bt]);
+            }
           }
         } else {
           const int t = tbase + tt;
           const bool live = tt < nt && t < kend;
           if (MODE == MMode::kQkv) {
+            bool gok;
+            const v4u g = gamma_tile(live ? t : a.kt, gok);
 #pragma unroll
             for (int bt = 0; bt < NBT; ++bt) {
               float s2;
-              A[bt] = as_bf16x8(qkv_operand(ar[r][bt], g_chunk(t), live ? t : a.kt, bt, s2));
-              if (si == 0) ssp[bt] += s2;
+              A[bt] = as_bf16x8(qkv_operand(ar[r][bt], g, s2));
+              if (si == 0) ssp[bt] += gok ? s2 : 0.f;
             }
           } else {
             // a padding item (past the wave's run or the matrix) adds zero
