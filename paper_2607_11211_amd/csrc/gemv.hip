@@ -45,6 +45,11 @@ using gemv::max_chunks;
 using gemv::Mode;
 using gemv::segments_for;
 
+// floats before the input stage in a staged kernel's LDS (16-byte aligned)
+__host__ __device__ constexpr size_t staged_offset(size_t body_floats) { return (body_floats + 3) / 4 * 4; }
+// the largest LDS a staged launch takes (beyond it the waves load their own inputs)
+constexpr size_t kMaxStagedLds = 64 * 1024;
+
 template <int BT, int MAXCH, int NSEG_H, int NBUF, Mode MODE>
 __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
@@ -53,6 +58,26 @@ __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
   body.load_inputs();
   __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
   body.prime();
+  body.run();
+}
+
+// One sequence with its inputs staged in LDS: the block loads the activation
+// and the gains once (InputStage), issues its first weight rows behind them,
+// and its waves take their chunks from the stage.
+template <int MAXCH, int NSEG_H, int NBUF, Mode MODE>
+__global__ __launch_bounds__(kWaves * kWave) void gemv_staged_kernel(GemvArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  using Body = gemv::GemvBody<1, MAXCH, NSEG_H, NBUF, MODE, gemv::GlobalIO>;
+  Body body(a, gemv::GlobalIO{}, lds, blockIdx.x, gridDim.x, 0, threadIdx.x);
+  v4u* stage = reinterpret_cast<v4u*>(lds + staged_offset(Body::lds_floats(a.rows, gridDim.x)));
+  gemv::InputStage<MODE> st;
+  st.load(a, threadIdx.x);
+  body.load_resid();
+  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
+  body.prime();
+  st.store(stage);
+  __syncthreads();
+  body.load_act_lds(stage);
   body.run();
 }
 
@@ -70,8 +95,14 @@ hipError_t launch_shape(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
       BT * ((((a.rows + nblk - 1) / nblk) + NG - 1) / NG) > kWave)
     return hipErrorInvalidValue;
   dim3 grid(nblk, (a.batch + BT - 1) / BT);
-  const size_t lds =
-      ((size_t)halves<MODE>() * NSEG_H * BT * ((a.rows + nblk - 1) / nblk) + (size_t)NSEG_H * BT) * sizeof(float);
+  const size_t body_floats = (size_t)halves<MODE>() * NSEG_H * BT * ((a.rows + nblk - 1) / nblk) + (size_t)NSEG_H * BT;
+  if constexpr (BT == 1 && MODE != Mode::kPlain) {
+    using Stage = gemv::InputStage<MODE>;
+    const size_t lds = staged_offset(body_floats) * sizeof(float) + (size_t)Stage::pieces(a.din) * sizeof(v4u);
+    if (Stage::fits(a.din) && lds <= kMaxStagedLds)
+      return ext_launch(gemv_staged_kernel<MAXCH, NSEG_H, NBUF, MODE>, grid, dim3(kWaves * kWave), lds, s, ev, a);
+  }
+  const size_t lds = body_floats * sizeof(float);
   return ext_launch(gemv_kernel<BT, MAXCH, NSEG_H, NBUF, MODE>, grid, dim3(kWaves * kWave), lds, s, ev, a);
 }
 

@@ -176,6 +176,27 @@ struct GemvBody {
     }
   }
 
+  // the same from a block's LDS stage of one sequence (BT 1): 16-byte pieces,
+  // the activation's (fp32, or bf16 x in the QKV mode) first, then the gains'
+  __device__ __forceinline__ void load_act_lds(const v4u* stage) {
+    static_assert(BT == 1, "one sequence per stage");
+    const int nact = MODE == Mode::kNormQkv ? nch : 2 * nch;
+#pragma unroll
+    for (int j = 0; j < MAXCH; ++j) {
+      const int c = min(cbase + lane + kWave * j, nch - 1);
+      if (MODE == Mode::kNormQkv) {
+        xr[0][j] = stage[c];
+      } else {
+        const v4u u0 = stage[2 * c], u1 = stage[2 * c + 1];
+        fr[0][j][0] = make_float4(__uint_as_float(u0.x), __uint_as_float(u0.y), __uint_as_float(u0.z),
+                                  __uint_as_float(u0.w));
+        fr[0][j][1] = make_float4(__uint_as_float(u1.x), __uint_as_float(u1.y), __uint_as_float(u1.z),
+                                  __uint_as_float(u1.w));
+      }
+      if (has_norm<MODE>()) gr[j] = stage[nact + c];
+    }
+  }
+
   // ---- 2. the ring's first NBUF rows ----------------------------------------
   __device__ __forceinline__ void prime() {
 #pragma unroll
@@ -309,6 +330,47 @@ struct GemvBody {
         else io.out(a, o, v[0]);
       }
     }
+  }
+};
+
+// The inputs of one sequence staged in LDS by the whole block: the activation
+// (fp32 [din], or the token x as bf16 in the QKV mode) and the RMSNorm gains
+// (bf16 [din]) as 16-byte pieces, piece p loaded by thread p mod kThreads.
+// Each element then crosses the CU's load path once per block instead of
+// once per wave group that uses it (the waves of a row's two halves and of
+// every group of rows read the same chunks).
+template <Mode MODE>
+struct InputStage {
+  static constexpr int kThreads = kWaves * kWave;
+  static constexpr int kMaxPieces = 4;  // per thread
+  v4u v[kMaxPieces];
+  int n, nact, per, tid;
+
+  static __host__ __device__ int act_pieces(int din) { return MODE == Mode::kNormQkv ? din / 8 : din / 4; }
+  static __host__ __device__ int pieces(int din) { return act_pieces(din) + (has_norm<MODE>() ? din / 8 : 0); }
+  static __host__ __device__ bool fits(int din) { return pieces(din) <= kMaxPieces * kThreads; }
+
+  // the loads (every one clamped to a piece that exists; `per` is uniform)
+  __device__ __forceinline__ void load(const GemvArgs& a, int tid_) {
+    tid = tid_;
+    nact = act_pieces(a.din);
+    n = pieces(a.din);
+    per = (n + kThreads - 1) / kThreads;
+    const v4u* act = MODE == Mode::kNormQkv ? reinterpret_cast<const v4u*>(a.x_bf16)
+                                            : reinterpret_cast<const v4u*>(a.in_f32);
+    const v4u* g = reinterpret_cast<const v4u*>(a.gamma);
+#pragma unroll
+    for (int i = 0; i < kMaxPieces; ++i)
+      if (i < per) {
+        const int q = min(tid + kThreads * i, n - 1);
+        v[i] = has_norm<MODE>() && q >= nact ? g[q - nact] : act[q];
+      }
+  }
+
+  __device__ __forceinline__ void store(v4u* stage) const {
+#pragma unroll
+    for (int i = 0; i < kMaxPieces; ++i)
+      if (i < per && tid + kThreads * i < n) stage[tid + kThreads * i] = v[i];
   }
 };
 
