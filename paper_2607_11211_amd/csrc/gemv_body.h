@@ -73,6 +73,23 @@ __device__ __forceinline__ void dot_slot(float (&acc)[BT], const v4u (&w)[MAXCH]
   }
 }
 
+// dot_slot for chunk j alone
+template <int BT, int MAXCH>
+__device__ __forceinline__ void dot_chunk(float (&acc)[BT], const v4u& w, const float (&act)[BT][MAXCH][8], int j,
+                                          int nch, int cbase, int lane) {
+  if (cbase + lane + kWave * j < nch) {
+    float wf[8];
+    unpack8(w, wf);
+#pragma unroll
+    for (int b = 0; b < BT; ++b) {
+      float s = acc[b];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s = fmaf(wf[e], act[b][j][e], s);
+      acc[b] = s;
+    }
+  }
+}
+
 // Global-memory IO of the separate kernels.
 struct GlobalIO {
   // float4 i4 of activation row b
@@ -262,14 +279,30 @@ struct GemvBody {
     float acc[BT];
 #pragma unroll
     for (int b = 0; b < BT; ++b) acc[b] = 0.f;
+    // one row in flight: the next row's chunk j goes out as soon as this
+    // row's chunk j has been used (the row pointers advance by a fixed step)
+    const v4u* rbase = W + (size_t)(blk + G * grp) * row_chunks + hoff;
+    const size_t rstep = (size_t)G * NG * row_chunks;
+    const v4u* rdeadp = W + (size_t)rdead * row_chunks;
     for (int k0 = 0; k0 < nmine; k0 += NBUF) {
 #pragma unroll
       for (int s = 0; s < NBUF; ++s) {
         const int k = k0 + s;
         const bool live = k < nmine;
-        if (live) dot_slot<BT, MAXCH>(acc, w[s], act, nch, cbase, lane);
-        load_slot<MAXCH>(w[s], W, row_chunks, k + NBUF < nmine, blk + G * (grp + NG * (k + NBUF)), rdead, hoff, nch,
-                         cbase, lane);
+        if constexpr (NBUF == 1) {
+          const bool nlive = k + 1 < nmine;
+          const v4u* nrow = nlive ? rbase + (size_t)(k + 1) * rstep : rdeadp;
+          const int ncmax = nlive ? nch - 1 : 0;
+#pragma unroll
+          for (int j = 0; j < MAXCH; ++j) {
+            if (live) dot_chunk<BT, MAXCH>(acc, w[0][j], act, j, nch, cbase, lane);
+            w[0][j] = ld_stream(nrow + min(cbase + lane + kWave * j, ncmax));
+          }
+        } else {
+          if (live) dot_slot<BT, MAXCH>(acc, w[s], act, nch, cbase, lane);
+          load_slot<MAXCH>(w[s], W, row_chunks, k + NBUF < nmine, blk + G * (grp + NG * (k + NBUF)), rdead, hoff,
+                           nch, cbase, lane);
+        }
         if (live) {
           const int i = grp + NG * k;  // block-local row
 #pragma unroll
