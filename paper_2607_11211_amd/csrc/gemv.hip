@@ -63,21 +63,23 @@ __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
 
 // One sequence with its inputs staged in LDS: the block loads the activation
 // and the gains once (InputStage), issues its first weight rows behind them,
-// and its waves take their chunks from the stage.
+// and its waves take their chunks from the stage; the norm's sum of squares
+// is summed while the stage is stored (one block barrier for both).
 template <int MAXCH, int NSEG_H, int NBUF, Mode MODE>
 __global__ __launch_bounds__(kWaves * kWave) void gemv_staged_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   using Body = gemv::GemvBody<1, MAXCH, NSEG_H, NBUF, MODE, gemv::GlobalIO>;
   Body body(a, gemv::GlobalIO{}, lds, blockIdx.x, gridDim.x, 0, threadIdx.x);
-  v4u* stage = reinterpret_cast<v4u*>(lds + staged_offset(Body::lds_floats(a.rows, gridDim.x)));
+  float* wss = lds + staged_offset(Body::lds_floats(a.rows, gridDim.x));  // [kWaves]
+  v4u* stage = reinterpret_cast<v4u*>(wss + kWaves);
   gemv::InputStage<MODE> st;
   st.load(a, threadIdx.x);
   body.load_resid();
   __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
   body.prime();
-  st.store(stage);
+  st.store(stage, wss);
   __syncthreads();
-  body.load_act_lds(stage);
+  body.load_act_lds(stage, wss);
   body.run();
 }
 
@@ -98,7 +100,8 @@ hipError_t launch_shape(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
   const size_t body_floats = (size_t)halves<MODE>() * NSEG_H * BT * ((a.rows + nblk - 1) / nblk) + (size_t)NSEG_H * BT;
   if constexpr (BT == 1 && MODE != Mode::kPlain) {
     using Stage = gemv::InputStage<MODE>;
-    const size_t lds = staged_offset(body_floats) * sizeof(float) + (size_t)Stage::pieces(a.din) * sizeof(v4u);
+    const size_t lds =
+        (staged_offset(body_floats) + kWaves) * sizeof(float) + (size_t)Stage::pieces(a.din) * sizeof(v4u);
     if (Stage::fits(a.din) && lds <= kMaxStagedLds)
       return ext_launch(gemv_staged_kernel<MAXCH, NSEG_H, NBUF, MODE>, grid, dim3(kWaves * kWave), lds, s, ev, a);
   }

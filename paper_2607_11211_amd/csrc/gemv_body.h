@@ -124,6 +124,8 @@ struct GemvBody {
   bool resid_reg;
   const v4u* W;
   float resid;
+  float ss_in;    // staged inputs: the row's sum of squares for the norm
+  bool ss_given;  // (computed by the stage, so run() does not)
   v4u xr[BT][MAXCH];        // x chunks (bf16), QKV norm mode
   float4 fr[BT][MAXCH][2];  // fp32 activation chunks, other modes
   v4u gr[MAXCH];            // gain chunks
@@ -155,6 +157,8 @@ struct GemvBody {
     ssq = lds + (size_t)NSEG * BT * nres;
     W = reinterpret_cast<const v4u*>(a.w);
     resid = 0.f;
+    ss_in = 0.f;
+    ss_given = false;
   }
 
   // ---- 1. residuals of this wave's rows, its activation chunks, the gains --
@@ -195,9 +199,17 @@ struct GemvBody {
 
   // the same from a block's LDS stage of one sequence (BT 1): 16-byte pieces,
   // the activation's (fp32, or bf16 x in the QKV mode) first, then the gains'
-  __device__ __forceinline__ void load_act_lds(const v4u* stage) {
+  // (wss: the stage's per-wave sums of squares, added here in wave order)
+  __device__ __forceinline__ void load_act_lds(const v4u* stage, const float* wss) {
     static_assert(BT == 1, "one sequence per stage");
     const int nact = MODE == Mode::kNormQkv ? nch : 2 * nch;
+    if (has_norm<MODE>()) {
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) t += wss[w];
+      ss_in = t;
+      ss_given = true;
+    }
 #pragma unroll
     for (int j = 0; j < MAXCH; ++j) {
       const int c = min(cbase + lane + kWave * j, nch - 1);
@@ -238,27 +250,33 @@ struct GemvBody {
       // RMSNorm: x / sqrt(mean(x^2) + eps) * gamma over the full row; a row
       // cut into segments adds its segments' sums of squares through LDS
       float ss[BT];
+      if (ss_given) {
+        // staged inputs: the stage summed the squares (uniform branch)
 #pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        float t = 0.f;
-#pragma unroll
-        for (int j = 0; j < MAXCH; ++j)
-          if (cbase + lane + kWave * j < nch)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) t = fmaf(src(b, j, e), src(b, j, e), t);
-        ss[b] = wave_sum(t);
-      }
-      if (NSEG_H > 1) {
-        if (grp == 0 && half == 0 && lane == 0)
-#pragma unroll
-          for (int b = 0; b < BT; ++b) ssq[sh * BT + b] = ss[b];
-        __syncthreads();
+        for (int b = 0; b < BT; ++b) ss[b] = ss_in;
+      } else {
 #pragma unroll
         for (int b = 0; b < BT; ++b) {
           float t = 0.f;
 #pragma unroll
-          for (int i = 0; i < NSEG_H; ++i) t += ssq[i * BT + b];
-          ss[b] = t;
+          for (int j = 0; j < MAXCH; ++j)
+            if (cbase + lane + kWave * j < nch)
+#pragma unroll
+              for (int e = 0; e < 8; ++e) t = fmaf(src(b, j, e), src(b, j, e), t);
+          ss[b] = wave_sum(t);
+        }
+        if (NSEG_H > 1) {
+          if (grp == 0 && half == 0 && lane == 0)
+#pragma unroll
+            for (int b = 0; b < BT; ++b) ssq[sh * BT + b] = ss[b];
+          __syncthreads();
+#pragma unroll
+          for (int b = 0; b < BT; ++b) {
+            float t = 0.f;
+#pragma unroll
+            for (int i = 0; i < NSEG_H; ++i) t += ssq[i * BT + b];
+            ss[b] = t;
+          }
         }
       }
 #pragma unroll
@@ -400,10 +418,32 @@ struct InputStage {
       }
   }
 
-  __device__ __forceinline__ void store(v4u* stage) const {
+  // the pieces into the stage; for the norm modes also the sum of squares of
+  // this wave's activation pieces into wss[wave] (kWaves floats of LDS)
+  __device__ __forceinline__ void store(v4u* stage, float* wss) const {
+    float t = 0.f;
 #pragma unroll
     for (int i = 0; i < kMaxPieces; ++i)
-      if (i < per && tid + kThreads * i < n) stage[tid + kThreads * i] = v[i];
+      if (i < per && tid + kThreads * i < n) {
+        stage[tid + kThreads * i] = v[i];
+        if (has_norm<MODE>() && tid + kThreads * i < nact) {
+          if (MODE == Mode::kNormQkv) {
+            float f[8];
+            unpack8(v[i], f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t = fmaf(f[e], f[e], t);
+          } else {
+            const float f[4] = {__uint_as_float(v[i].x), __uint_as_float(v[i].y), __uint_as_float(v[i].z),
+                                __uint_as_float(v[i].w)};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) t = fmaf(f[e], f[e], t);
+          }
+        }
+      }
+    if (has_norm<MODE>()) {
+      t = wave_sum(t);
+      if ((tid & (kWave - 1)) == 0) wss[tid / kWave] = t;
+    }
   }
 };
 
