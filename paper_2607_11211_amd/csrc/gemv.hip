@@ -49,6 +49,8 @@ using gemv::segments_for;
 __host__ __device__ constexpr size_t staged_offset(size_t body_floats) { return (body_floats + 3) / 4 * 4; }
 // the largest LDS a staged launch takes (beyond it the waves load their own inputs)
 constexpr size_t kMaxStagedLds = 64 * 1024;
+// waves per block of the staged kernel where the row's segments fit (else 16)
+constexpr int kStagedWaves = 8;
 
 template <int BT, int MAXCH, int NSEG_H, int NBUF, Mode MODE>
 __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
@@ -64,15 +66,17 @@ __global__ __launch_bounds__(kWaves * kWave) void gemv_kernel(GemvArgs a) {
 // One sequence with its inputs staged in LDS: the block loads the activation
 // and the gains once (InputStage), issues its first weight rows behind them,
 // and its waves take their chunks from the stage; the norm's sum of squares
-// is summed while the stage is stored (one block barrier for both).
-template <int MAXCH, int NSEG_H, int NBUF, Mode MODE>
-__global__ __launch_bounds__(kWaves * kWave) void gemv_staged_kernel(GemvArgs a) {
+// is summed while the stage is stored (one block barrier for both). Blocks of
+// WAVES waves; with 8, two blocks share a CU (at most 128 registers a lane).
+template <int MAXCH, int NSEG_H, int NBUF, Mode MODE, int WAVES>
+__global__ __launch_bounds__(WAVES* kWave) __attribute__((amdgpu_waves_per_eu(4, 8))) void gemv_staged_kernel(
+    GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
-  using Body = gemv::GemvBody<1, MAXCH, NSEG_H, NBUF, MODE, gemv::GlobalIO>;
+  using Body = gemv::GemvBody<1, MAXCH, NSEG_H, NBUF, MODE, gemv::GlobalIO, WAVES>;
   Body body(a, gemv::GlobalIO{}, lds, blockIdx.x, gridDim.x, 0, threadIdx.x);
-  float* wss = lds + staged_offset(Body::lds_floats(a.rows, gridDim.x));  // [kWaves]
-  v4u* stage = reinterpret_cast<v4u*>(wss + kWaves);
-  gemv::InputStage<MODE> st;
+  float* wss = lds + staged_offset(Body::lds_floats(a.rows, gridDim.x));  // [WAVES]
+  v4u* stage = reinterpret_cast<v4u*>(wss + 16);
+  gemv::InputStage<MODE, WAVES> st;
   st.load(a, threadIdx.x);
   body.load_resid();
   __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weight loads
@@ -99,11 +103,25 @@ hipError_t launch_shape(const GemvArgs& a, hipStream_t s, KernelEvents ev) {
   dim3 grid(nblk, (a.batch + BT - 1) / BT);
   const size_t body_floats = (size_t)halves<MODE>() * NSEG_H * BT * ((a.rows + nblk - 1) / nblk) + (size_t)NSEG_H * BT;
   if constexpr (BT == 1 && MODE != Mode::kPlain) {
-    using Stage = gemv::InputStage<MODE>;
-    const size_t lds =
-        (staged_offset(body_floats) + kWaves) * sizeof(float) + (size_t)Stage::pieces(a.din) * sizeof(v4u);
+    constexpr int W2 = kStagedWaves;
+    if constexpr (halves<MODE>() * NSEG_H <= W2 / 2) {
+      using Stage = gemv::InputStage<MODE, W2>;
+      const int nblk2 = a.rows < kNumCu * (kWaves / W2) ? a.rows : kNumCu * (kWaves / W2);
+      const size_t bf2 =
+          (size_t)halves<MODE>() * NSEG_H * ((a.rows + nblk2 - 1) / nblk2) + (size_t)NSEG_H;
+      const size_t lds = (staged_offset(bf2) + 16) * sizeof(float) + (size_t)Stage::pieces(a.din) * sizeof(v4u);
+      constexpr int NG2 = W2 / (halves<MODE>() * NSEG_H);
+      const bool resid_ok = !(halves<MODE>() * NSEG_H == 1 && has_residual<MODE>() &&
+                              (((a.rows + nblk2 - 1) / nblk2) + NG2 - 1) / NG2 > kWave);
+      if (Stage::fits(a.din) && lds <= kMaxStagedLds && resid_ok)
+        return ext_launch(gemv_staged_kernel<MAXCH, NSEG_H, NBUF, MODE, W2>, dim3(nblk2), dim3(W2 * kWave), lds, s,
+                          ev, a);
+    }
+    using Stage = gemv::InputStage<MODE, kWaves>;
+    const size_t lds = (staged_offset(body_floats) + 16) * sizeof(float) + (size_t)Stage::pieces(a.din) * sizeof(v4u);
     if (Stage::fits(a.din) && lds <= kMaxStagedLds)
-      return ext_launch(gemv_staged_kernel<MAXCH, NSEG_H, NBUF, MODE>, grid, dim3(kWaves * kWave), lds, s, ev, a);
+      return ext_launch(gemv_staged_kernel<MAXCH, NSEG_H, NBUF, MODE, kWaves>, grid, dim3(kWaves * kWave), lds, s,
+                        ev, a);
   }
   const size_t lds = body_floats * sizeof(float);
   return ext_launch(gemv_kernel<BT, MAXCH, NSEG_H, NBUF, MODE>, grid, dim3(kWaves * kWave), lds, s, ev, a);

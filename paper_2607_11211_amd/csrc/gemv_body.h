@@ -100,13 +100,13 @@ struct GlobalIO {
   __device__ __forceinline__ void out(const GemvArgs& a, size_t o, float v) const { a.out[o] = v; }
 };
 
-template <int BT, int MAXCH, int NSEG_H, int NBUF, Mode MODE, class IO>
+template <int BT, int MAXCH, int NSEG_H, int NBUF, Mode MODE, class IO, int WAVES = kWaves>
 struct GemvBody {
   static constexpr int NH = halves<MODE>();
   static constexpr int NSEG = NH * NSEG_H;
-  static constexpr int NG = kWaves / NSEG;  // groups of waves
+  static constexpr int NG = WAVES / NSEG;  // groups of waves
   static constexpr int kSeg = kWave * MAXCH;
-  static_assert(NSEG <= kWaves && kWaves % NSEG == 0, "segments must divide the block's waves");
+  static_assert(NSEG <= WAVES && WAVES % NSEG == 0, "segments must divide the block's waves");
   static_assert(BT * MAXCH <= 6, "activation registers");
 
   // LDS words the body needs: part [NSEG][BT][nres] segment sums | ssq
@@ -206,7 +206,7 @@ struct GemvBody {
     if (has_norm<MODE>()) {
       float t = 0.f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) t += wss[w];
+      for (int w = 0; w < WAVES; ++w) t += wss[w];
       ss_in = t;
       ss_given = true;
     }
@@ -363,7 +363,7 @@ struct GemvBody {
     // ---- 5. rows cut into segments: add the segments (and siLu_Mul) -------
     if (NSEG > 1) {
       __syncthreads();
-      for (int t = tid; t < nb * nrow; t += kWaves * kWave) {
+      for (int t = tid; t < nb * nrow; t += WAVES * kWave) {
         const int b = t / nrow, i = t % nrow;
         float v[NH];
 #pragma unroll
@@ -390,9 +390,9 @@ struct GemvBody {
 // Each element then crosses the CU's load path once per block instead of
 // once per wave group that uses it (the waves of a row's two halves and of
 // every group of rows read the same chunks).
-template <Mode MODE>
+template <Mode MODE, int WAVES = kWaves>
 struct InputStage {
-  static constexpr int kThreads = kWaves * kWave;
+  static constexpr int kThreads = WAVES * kWave;
   static constexpr int kMaxPieces = 4;  // per thread
   v4u v[kMaxPieces];
   int n, nact, per, tid;
@@ -419,7 +419,7 @@ struct InputStage {
   }
 
   // the pieces into the stage; for the norm modes also the sum of squares of
-  // this wave's activation pieces into wss[wave] (kWaves floats of LDS)
+  // this wave's activation pieces into wss[wave] (WAVES floats of LDS)
   __device__ __forceinline__ void store(v4u* stage, float* wss) const {
     float t = 0.f;
 #pragma unroll
