@@ -192,6 +192,11 @@ struct GlobalIO {
 // XCH: the contiguous loads and the LDS exchange (bf16 caches; xk, xv each
 // hold kThreads / kWave spans of 16 RC rows, one per wave); otherwise each
 // lane loads its quarter rows itself with plain loads.
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
+
 template <int D, int G, int NRING, bool PBF16, int KVF, class IO, bool XCH = false>
 struct AttnBody {
   using R = LaneRow<D, KVF>;
@@ -279,8 +284,12 @@ struct AttnBody {
   }
 
   // this lane's quarter rows of ring slot r: the slot itself, or (XCH) its
-  // chunks through the wave's exchange spans (wave-private, so no barrier:
-  // a wave's LDS accesses take effect in program order)
+  // chunks through the wave's exchange spans (wave-private, so no block
+  // barrier: a wave's LDS accesses take effect in program order). A lane
+  // reads what other lanes wrote, which no per-lane dependence expresses, so
+  // wavefront-scope fences keep every write before the reads and the reads
+  // before the next slot's writes (without them the compiler may interleave
+  // them, and the exchange reads stale chunks)
   __device__ __forceinline__ void lane_rows(int r, Chunk (&kq)[NC], Chunk (&vq)[NC]) {
     if constexpr (XCH) {
       const int lane = tid % kWave;
@@ -289,12 +298,14 @@ struct AttnBody {
         xk[lane + kWave * c] = kr[r][c];
         xv[lane + kWave * c] = vr[r][c];
       }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       const int at = (lane >> 2) * RC + (lane & 3) * NC;
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         kq[c] = xk[at + c];
         vq[c] = xv[at + c];
       }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     } else {
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
@@ -375,27 +386,35 @@ struct AttnBody {
         }
       }
     };
-    for (int t0 = start; t0 < end; t0 += NRING * stride) {
+    // ring slot r holds tile tt: its update, and (REFILL) the slot's refill
+    // with the tile NRING further on (clamped past the end); the barrier keeps
+    // the refill after the unpack, so the new tile lands in the registers the
+    // old one leaves (no copies, no early waits)
+    auto slot = [&](int r, int tt, auto refill_tag) {
+      float kf[SEG], vf[SEG];
+      {
+        Chunk kq[NC], vq[NC];
+        lane_rows(r, kq, vq);
 #pragma unroll
-      for (int r = 0; r < NRING; ++r) {
-        const int tt = t0 + r * stride;
-        float kf[SEG], vf[SEG];
-        {
-          Chunk kq[NC], vq[NC];
-          lane_rows(r, kq, vq);
-#pragma unroll
-          for (int c = 0; c < NC; ++c) {
-            decode_chunk<KVF>(kq[c], kf + R::EPC * c);
-            decode_chunk<KVF>(vq[c], vf + R::EPC * c);
-          }
+        for (int c = 0; c < NC; ++c) {
+          decode_chunk<KVF>(kq[c], kf + R::EPC * c);
+          decode_chunk<KVF>(vq[c], vf + R::EPC * c);
         }
-        // refill the slot with the tile NRING further on (clamped past the end);
-        // the barrier keeps the refill after the unpack, so the new tile lands
-        // in the registers the old one leaves (no copies, no early waits)
-        __builtin_amdgcn_sched_barrier(0);
-        refill(r, tt + NRING * stride);
-        update(kf, vf, tt + j < end);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (decltype(refill_tag)::value) refill(r, tt + NRING * stride);
+      update(kf, vf, tt + j < end);
+    };
+    // the last round refills nothing: its refills would be loads past the
+    // split that the merge below waits for (it reuses their registers)
+    int t0 = start;
+    for (; t0 + NRING * stride < end; t0 += NRING * stride) {
+#pragma unroll
+      for (int r = 0; r < NRING; ++r) slot(r, t0 + r * stride, BoolTag<true>{});
+    }
+    if (t0 < end) {
+#pragma unroll
+      for (int r = 0; r < NRING; ++r) slot(r, t0 + r * stride, BoolTag<false>{});
     }
     // the new entry N_p (Eq. 1 slot) from the rounded values in LDS, by the
     // four lanes of position 0

@@ -298,48 +298,58 @@ struct GemvBody {
 #pragma unroll
     for (int b = 0; b < BT; ++b) acc[b] = 0.f;
     // one row in flight: the next row's chunk j goes out as soon as this
-    // row's chunk j has been used (the row pointers advance by a fixed step)
+    // row's chunk j has been used (the row pointers advance by a fixed step);
+    // the last row issues nothing, so nothing after the loop waits for loads
+    // whose data is never used
     const v4u* rbase = W + (size_t)(blk + G * grp) * row_chunks + hoff;
     const size_t rstep = (size_t)G * NG * row_chunks;
-    const v4u* rdeadp = W + (size_t)rdead * row_chunks;
-    for (int k0 = 0; k0 < nmine; k0 += NBUF) {
+    // the wave's k-th row is summed in acc: its outputs, or its segment's part
+    auto finish = [&](int k) {
+      const int i = grp + NG * k;  // block-local row
 #pragma unroll
-      for (int s = 0; s < NBUF; ++s) {
-        const int k = k0 + s;
-        const bool live = k < nmine;
-        if constexpr (NBUF == 1) {
-          const bool nlive = k + 1 < nmine;
-          const v4u* nrow = nlive ? rbase + (size_t)(k + 1) * rstep : rdeadp;
-          const int ncmax = nlive ? nch - 1 : 0;
+      for (int b = 0; b < BT; ++b) {
+        // batch rows past the tile's end repeat its last row, value and
+        // address alike, so every store below is unconditional
+        const int bs = min(b, nb - 1);
+        float v = wave_sum(acc[b]);
+        acc[b] = 0.f;
+        if (has_residual<MODE>() && seg == 0 && resid_reg)
+          v += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(resid), bs * nmine + k));
+        if (NSEG == 1) {
+          const size_t o = (size_t)(b0 + bs) * a.rows + blk + (size_t)G * i;
+          if (MODE == Mode::kDownResidual) a.out_bf16[o] = f32_to_bf16(v);
+          else io.out(a, o, v);
+        } else if (lane == 0) {
+          part[((size_t)seg * BT + b) * nres + i] = v;
+        }
+      }
+    };
+    if constexpr (NBUF == 1) {
+      int k = 0;
+      for (; k + 1 < nmine; ++k) {
+        const v4u* nrow = rbase + (size_t)(k + 1) * rstep;
 #pragma unroll
-          for (int j = 0; j < MAXCH; ++j) {
-            if (live) dot_chunk<BT, MAXCH>(acc, w[0][j], act, j, nch, cbase, lane);
-            w[0][j] = ld_stream(nrow + min(cbase + lane + kWave * j, ncmax));
-          }
-        } else {
+        for (int j = 0; j < MAXCH; ++j) {
+          dot_chunk<BT, MAXCH>(acc, w[0][j], act, j, nch, cbase, lane);
+          w[0][j] = ld_stream(nrow + min(cbase + lane + kWave * j, nch - 1));
+        }
+        finish(k);
+      }
+      if (k < nmine) {
+#pragma unroll
+        for (int j = 0; j < MAXCH; ++j) dot_chunk<BT, MAXCH>(acc, w[0][j], act, j, nch, cbase, lane);
+        finish(k);
+      }
+    } else {
+      for (int k0 = 0; k0 < nmine; k0 += NBUF) {
+#pragma unroll
+        for (int s = 0; s < NBUF; ++s) {
+          const int k = k0 + s;
+          const bool live = k < nmine;
           if (live) dot_slot<BT, MAXCH>(acc, w[s], act, nch, cbase, lane);
           load_slot<MAXCH>(w[s], W, row_chunks, k + NBUF < nmine, blk + G * (grp + NG * (k + NBUF)), rdead, hoff,
                            nch, cbase, lane);
-        }
-        if (live) {
-          const int i = grp + NG * k;  // block-local row
-#pragma unroll
-          for (int b = 0; b < BT; ++b) {
-            // batch rows past the tile's end repeat its last row, value and
-            // address alike, so every store below is unconditional
-            const int bs = min(b, nb - 1);
-            float v = wave_sum(acc[b]);
-            acc[b] = 0.f;
-            if (has_residual<MODE>() && seg == 0 && resid_reg)
-              v += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(resid), bs * nmine + k));
-            if (NSEG == 1) {
-              const size_t o = (size_t)(b0 + bs) * a.rows + blk + (size_t)G * i;
-              if (MODE == Mode::kDownResidual) a.out_bf16[o] = f32_to_bf16(v);
-              else io.out(a, o, v);
-            } else if (lane == 0) {
-              part[((size_t)seg * BT + b) * nres + i] = v;
-            }
-          }
+          if (live) finish(k);
         }
       }
     }
