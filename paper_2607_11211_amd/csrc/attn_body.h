@@ -192,11 +192,6 @@ struct GlobalIO {
 // XCH: the contiguous loads and the LDS exchange (bf16 caches; xk, xv each
 // hold kThreads / kWave spans of 16 RC rows, one per wave); otherwise each
 // lane loads its quarter rows itself with plain loads.
-template <bool B>
-struct BoolTag {
-  static constexpr bool value = B;
-};
-
 template <int D, int G, int NRING, bool PBF16, int KVF, class IO, bool XCH = false>
 struct AttnBody {
   using R = LaneRow<D, KVF>;

@@ -9,6 +9,13 @@ namespace fasttps {
 
 constexpr int kWave = 64;
 
+// a compile-time flag passed to a generic lambda (the body of a loop's last
+// round and of the rounds before it)
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
+
 // 16 bytes as a native vector: copies of it are plain vector moves, so
 // staging arrays of it stay in registers (HIP's uint4 struct is copied with
 // memcpy, which can pin such arrays to scratch memory).

@@ -411,7 +411,11 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
   float* kp_own = ks > 1 ? a.kpart + ((size_t)blockIdx.y * G + blk) * a.kstride : nullptr;
   // stripe si (its partial sums into LDS; the epilogue after the last stripe
   // of a chunk)
-  auto stripe = [&](int si) {
+  // LAST (the block's last stripe): refill only items of this stripe; the
+  // refills past it would be clamped loads that nothing uses, and the
+  // epilogue would wait for them (it reuses their registers)
+  auto stripe = [&](int si, auto last_tag) {
+    constexpr bool LAST = decltype(last_tag)::value;
     f4 acc[NBT];
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) acc[bt] = f4{0.f, 0.f, 0.f, 0.f};
@@ -484,7 +488,7 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
         // the barrier keeps the refill after the MFMAs, so the new tile lands
         // in the registers the old one leaves (no copies, no early waits)
         __builtin_amdgcn_sched_barrier(0);
-        load_item(r, si * ntp + tt + NBUF);
+        if (!LAST || tt + NBUF < ntp) load_item(r, si * ntp + tt + NBUF);
       }
     }
 
@@ -545,7 +549,14 @@ __global__ __launch_bounds__(kMT) void mfma_proj_kernel(MfmaArgs a) {
     __syncthreads();
     c0 = si + 1;
   };
-  for (int si = 0; si < nstr; ++si) stripe(si);
+  // (the widest cached runs with two batch tiles keep one stripe body: a
+  // second copy of it spills there)
+  if constexpr (NBT == 2 && NT >= 7) {
+    for (int si = 0; si < nstr; ++si) stripe(si, BoolTag<false>{});
+  } else {
+    for (int si = 0; si + 1 < nstr; ++si) stripe(si, BoolTag<false>{});
+    stripe(nstr - 1, BoolTag<true>{});
+  }
 
   // ---- split inputs: the group's last block sums the parts in order -------
   if constexpr (MODE != MMode::kQkv) {
