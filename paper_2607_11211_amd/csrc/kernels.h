@@ -198,7 +198,9 @@ bool fused_layer_supported(const FusedShape& sh);
 int fused_layer_max_splits();  // attention splits per KV head the kernel merges
 int fused_layer_grid();        // its blocks (one (KV head, split) item each at most)
 hipError_t launch_fused_layer(const FusedArgs& f, const FusedShape& sh, hipStream_t s, KernelEvents ev = {});
-// the launch shape the separate GEMV kernels use for one sequence
+// the chunks per lane, segments per half row and ring depth the separate
+// GEMV kernels use for one sequence (their blocks have 8 or 16 waves; the
+// fused kernel's rows are dealt to its 16-wave blocks with the same shape)
 FusedShape::Gemv gemv_shape_b1(int din, bool gate_up);
 
 // The op-by-op baseline (Alg. 1 + Alg. 2, every intermediate through HBM).
