@@ -66,6 +66,10 @@ SMALL = [
                 intermediate=1024, rope_base=10000.0, max_seq=1100, pos=(1024,)),
     LayerConfig(name="s_merge17", index=26, batch=1, hidden=768, n_heads=8, n_kv_heads=8, head_dim=96,
                 intermediate=1024, rope_base=10000.0, max_seq=1100, pos=(1040,)),
+    # one sequence with inputs wider than the GEMVs' 64 KB LDS stage (the down projection's
+    # 20480 fp32 inputs): the unstaged GEMV kernel at one sequence
+    LayerConfig(name="s_wide_k", index=27, batch=1, hidden=512, n_heads=8, n_kv_heads=8, head_dim=64,
+                intermediate=20480, rope_base=10000.0, max_seq=200, pos=(150,)),
     # group 2, batch 9 (two batch tiles of the projections)
     LayerConfig(name="s_g2_b9", index=13, batch=9, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64,
                 intermediate=688, rope_base=10000.0, max_seq=200, pos=(0, 3, 17, 64, 100, 128, 150, 190, 199)),
