@@ -9,23 +9,27 @@
 //   * rows are dealt to the blocks round-robin (block b takes rows b, b + G,
 //     b + 2G, ... of a grid of G blocks), so at any moment the chip reads a
 //     compact window of the matrix;
-//   * a row is cut into NSEG segments of 64 MAXCH 16-byte chunks; the 16
-//     waves of a block form 16 / NSEG groups of NSEG waves, wave (g, s) taking
-//     segment s of the group's rows g, g + 16 / NSEG, ... Lane l of a wave
+//   * a row is cut into NSEG segments of 64 MAXCH 16-byte chunks; the W
+//     waves of a block form W / NSEG groups of NSEG waves, wave (g, s) taking
+//     segment s of the group's rows g, g + W / NSEG, ... Lane l of a wave
 //     reads chunks l, l + 64, ... of its segment, so every load instruction
-//     covers one contiguous kilobyte;
+//     covers one contiguous kilobyte. W = 16 (one block per CU), or at one
+//     sequence and rows of up to four segments W = 8 with two blocks per CU;
 //   * each wave holds the activation values of its own chunks in registers
-//     (fp32), loaded before its first weight load: a wave's loads return in
-//     the order they were issued, so the activation is ready as soon as the
-//     first weight row is, and no wave waits for another before it computes
-//     (only a row cut into segments needs the block's waves to meet: its
-//     sum of squares for the norm, and its segment sums, go through LDS);
+//     (fp32). At one sequence the block first stages the activation and the
+//     gains in LDS (one load per 16 bytes per block, issued ahead of the
+//     weight rows, the norm's sum of squares summed on the way) and the waves
+//     read their chunks from there; otherwise each wave loads its chunks
+//     itself before its first weight load. Only a row cut into segments
+//     needs the block's waves to meet again, for its segment sums;
 //   * each wave keeps NBUF rows in flight (2-4 KB): more outstanding loads
-//     per CU only queue up in the memory system;
-//   * every global load is issued unconditionally (clamped or dead addresses
-//     where there is nothing to load), so the number of loads in flight is
-//     the same on every path and the compiler waits for exactly the ring
-//     slot a dot product needs.
+//     per CU only queue up in the memory system. With one row in flight the
+//     next row's chunk j is issued right after chunk j is used, and the last
+//     row issues nothing;
+//   * every global load of the stream is issued unconditionally (clamped or
+//     dead addresses where there is nothing to load), so the number of loads
+//     in flight is the same on every path and the compiler waits for exactly
+//     the ring slot a dot product needs.
 // The gate/up projection reads the interlaced W_gu (Section 3.2 item 1,
 // Alg. 4) with tiles of one row: row 2k is gate row k and row 2k+1 up row k,
 // so one row of this kernel is the pair [gate k | up k] of 2D values, its two

@@ -5,6 +5,8 @@
 // The body keeps its state in registers (a struct that never leaves the
 // kernel) and runs in three steps:
 //   load_inputs()  residuals, the activation chunks of this wave and the gains
+//                  (or load_resid(), then load_act_lds() from a block's
+//                  InputStage once the stage is in LDS)
 //   prime()        the ring's first NBUF rows (weights do not depend on the
 //                  activation, so a fused kernel primes them before it waits
 //                  for the phase that produces the activation)
