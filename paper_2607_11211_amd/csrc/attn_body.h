@@ -465,23 +465,34 @@ struct AttnBody {
     __syncthreads();
 
     if (!live) return;
-    for (int i = tid; i < G * D; i += kThreads) {
+    // element i of the G heads' o by the lane pair (2i', 2i' + 1) of the
+    // block's threads, each lane over half of the 16 rows; the pair adds its
+    // halves with one lane swap (every thread takes part: the merge is the
+    // block's last step and nothing else hides its latency)
+    constexpr int kHalfRows = kRows / 2;
+    for (int i0 = 0; i0 < G * D; i0 += kThreads / 2) {
+      const int i = min(i0 + tid / 2, G * D - 1), hr = tid & 1;
       const int h = i / D, e = i % D;
       float M = sm.rm[h][0];
 #pragma unroll
       for (int r = 1; r < kRows; ++r) M = fmaxf(M, sm.rm[h][r]);
       float L = 0.f, O = 0.f;
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) {
+      for (int q = 0; q < kHalfRows; ++q) {
+        const int r = hr * kHalfRows + q;
         const float f = merge_factor(sm.rm[h][r], M);
         L = fmaf(sm.rl[h][r], f, L);
         O = fmaf(sm.red[h][r][e], f, O);
       }
-      float* pr = io.rec(a, b, g * G + h, s, D);
-      io.part(pr + kPartLead + e, KVF == kKvBf16 ? O : O * vscale);  // an 8-bit cache's V scale
-      if (e == 0) {
-        io.part(pr, M);
-        io.part(pr + 1, L);
+      L += dpp_mov<kDppQuadXor1>(L);
+      O += dpp_mov<kDppQuadXor1>(O);
+      if (hr == 0 && i0 + tid / 2 < G * D) {
+        float* pr = io.rec(a, b, g * G + h, s, D);
+        io.part(pr + kPartLead + e, KVF == kKvBf16 ? O : O * vscale);  // an 8-bit cache's V scale
+        if (e == 0) {
+          io.part(pr, M);
+          io.part(pr + 1, L);
+        }
       }
     }
   }
