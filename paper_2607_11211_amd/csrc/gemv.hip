@@ -211,17 +211,26 @@ __global__ __launch_bounds__(kMergeThreads) void oproj_merge_kernel(GemvArgs a, 
   float* stage = lds;            // o [H d]
   float* gl = lds + nel;
 
-  // (1) the partials (clamped, unconditional loads; o is 16-byte aligned in
-  // every record and D is a multiple of 4, so the four elements share a head)
+  // (1) the partials (o is 16-byte aligned in every record and D is a
+  // multiple of 4, so the four elements share a head); threads past the last
+  // element load nothing (whole waves of them skip the loads)
+  const bool has_e = tid < nel / 4;
   const int e = 4 * min(tid, nel / 4 - 1);
   const float* ph = m.part + (size_t)(e / D) * m.nsplit_cap * rs;
   float4 ov[NS];
   float2 ml[NS];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    const float* r = ph + (size_t)min(s, ns - 1) * rs;
-    ml[s] = *reinterpret_cast<const float2*>(r);
-    ov[s] = *reinterpret_cast<const float4*>(r + kPartLead + e % D);
+    ml[s] = make_float2(0.f, 0.f);
+    ov[s] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (has_e) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const float* r = ph + (size_t)min(s, ns - 1) * rs;
+      ml[s] = *reinterpret_cast<const float2*>(r);
+      ov[s] = *reinterpret_cast<const float4*>(r + kPartLead + e % D);
+    }
   }
   gemv::GemvBody<1, MAXCH, NSEG_H, NBUF, Mode::kResidual, StageIO> body(a, StageIO{stage}, gl, blockIdx.x, gridDim.x,
                                                                         0, tid);
@@ -245,7 +254,7 @@ __global__ __launch_bounds__(kMergeThreads) void oproj_merge_kernel(GemvArgs a, 
     acc.z = fmaf(ov[s].z, f, acc.z);
     acc.w = fmaf(ov[s].w, f, acc.w);
   }
-  if (tid < nel / 4) {
+  if (has_e) {
     const float4 v = make_float4(acc.x / L, acc.y / L, acc.z / L, acc.w / L);
     *reinterpret_cast<float4*>(stage + e) = v;
     if (blockIdx.x == 0) *reinterpret_cast<float4*>(m.o + e) = v;
