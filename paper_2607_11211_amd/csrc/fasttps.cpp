@@ -790,7 +790,7 @@ int run_step(fasttps_layer* l, const fasttps_weights* w, const void* x, const in
   // (FASTTPS_GEMM_FUSED), where it is built for the shape and the step is the
   // plain bf16-cache step. Not the automatic choice: on MI355X its phase
   // hand-overs through coherent flags cost more than the separate kernels'
-  // boundaries in a HIP graph (67.6 vs 57.7 us per Phi-3 layer at KV 4096).
+  // boundaries in a HIP graph (69.6 vs 54.4 us per Phi-3 layer at KV 4096).
   FusedShape fsh{};
   fsh.head_dim = (int)d;
   fsh.group = c.n_heads / c.n_kv_heads;
